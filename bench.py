@@ -1,0 +1,184 @@
+"""Benchmark of the packed whole+shard attention hot path on one MI355X.
+
+One step = the whole path over one packed batch: one forward launch over the
+WHOLE and SHARD segments together, the LSE merge of the shard partials, and
+the backward (preprocess, main, dQ finalize), inputs resident in HBM.  The
+default workload is the coalesced whole+shard batch: one GPU's share of a
+75,600-token 720p video at CP=8 (a 9450-query shard against all 8 K/V blocks
+of 9450 tokens) packed with six whole 1560-token images, 40 heads, d=128,
+bf16.  It is the one batch that exercises every step of the path.
+
+Prints one JSON line.  value = fwd+bwd TFLOP/s with the FlashAttention FLOP
+convention (forward 4*d*H*pairs, backward 10*d*H*pairs, pairs = block-diagonal
+query-key pairs only).  roofline = the dominant kernel (backward main) timed
+with HIP events on its own stream inside the timed region, priced at its
+algorithmic 8*d*H*pairs FLOPs against the bf16 dense MFMA peak.
+cpu_baseline = the fp64 oracle timed on this host's cores on a bounded
+sample of the same batch (see --cpu-sample-heads).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+METRIC = "packed whole+shard attention fwd+bwd TFLOP/s (bf16) and % of MFMA peak"
+BF16_PEAK_TFLOPS = 2516.6      # 256 CU x 2.4 GHz x 4096 bf16 FLOP/clk/CU (dense)
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c4", help="c2..c5 (default c4: coalesced whole+shard)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-heads", type=int, default=1)
+    return ap.parse_args()
+
+
+def cpu_baseline(w, heads):
+    """Time the oracle (as it stands) on a bounded sample of workload w.
+
+    Sample: `heads` head(s); every whole segment in full (forward+backward);
+    each shard reduced to its first 1/9 of query rows, forward against all of
+    its blocks, merge, and backward against all blocks.  FLOPs are counted
+    with the same convention as the GPU value (14*d per pair).
+    """
+    import numpy as np
+    import oracle
+    from paper_2608_01150_amd import workloads as W
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count() or 1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    hs = list(range(heads))
+    d = w.desc_dict()
+    cq = list(d["cu_seqlens_q"])
+    # shrink shard query rows: keep the first ceil(L/9) rows of each shard
+    new_cq, rows = [0], []
+    for s in range(w.num_segments):
+        a, b = cq[s], cq[s + 1]
+        if w.kind[s] == W.SHARD:
+            b = a + (b - a + 8) // 9
+        rows.append((a, b))
+        new_cq.append(new_cq[-1] + (b - a))
+    d2 = dict(d, cu_seqlens_q=tuple(new_cq))
+    q = np.concatenate([w.slice(W.TENSOR_Q, a, b, heads=hs).double().numpy() for a, b in rows])
+    do = np.concatenate([w.slice(W.TENSOR_DO, a, b, heads=hs).double().numpy() for a, b in rows])
+    k = w.slice(W.TENSOR_K, 0, w.total_k, heads=hs).double().numpy()
+    v = w.slice(W.TENSOR_V, 0, w.total_k, heads=hs).double().numpy()
+    pairs = 0
+    for s in range(w.num_segments):
+        lq = new_cq[s + 1] - new_cq[s]
+        for j in range(w.kv_first[s], w.kv_first[s] + w.kv_count[s]):
+            pairs += lq * (w.cu_seqlens_k[j + 1] - w.cu_seqlens_k[j])
+    t0 = time.perf_counter()
+    fwd = oracle.packed_forward(d2, q, k, v, w.scale)
+    for s in range(w.num_segments):
+        if w.kind[s] == W.SHARD:
+            a, b = new_cq[s], new_cq[s + 1]
+            for h in range(len(hs)):
+                oracle.lse_merge(fwd["o_part"][:, a:b, h], fwd["lse_part"][:, a:b, h])
+    oracle.packed_backward(d2, q, k, v, do, w.scale)
+    dt = time.perf_counter() - t0
+    flops = 14.0 * w.head_dim * len(hs) * pairs
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{len(hs)} of {w.num_heads} heads; whole segments in full, each shard's first 1/9 of "
+                      f"query rows against all blocks; fwd+merge+bwd fp64; {pairs} pairs/head, {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build measures one GPU's share of the batch "
+              "(context parallelism is simulated by feeding that GPU's K/V blocks locally); "
+              "--gpus must be 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2608_01150_amd import api
+    from paper_2608_01150_amd import workloads as W
+
+    w = W.get(args.workload)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    desc = api.SegDesc.of(w)
+    H, hd = w.num_heads, w.head_dim
+    q = w.full(W.TENSOR_Q, device=dev)
+    k = w.full(W.TENSOR_K, device=dev)
+    v = w.full(W.TENSOR_V, device=dev)
+    do = w.full(W.TENSOR_DO, device=dev)
+    out = torch.empty_like(q)
+    lse = torch.empty((w.total_q, H), dtype=torch.float32, device=dev)
+    o_part = lse_part = None
+    if w.num_slots:
+        o_part = torch.empty((w.num_slots, w.total_q, H, hd), dtype=torch.float32, device=dev)
+        lse_part = torch.empty((w.num_slots, w.total_q, H), dtype=torch.float32, device=dev)
+    dq = torch.empty_like(q)
+    dk = torch.empty_like(k)
+    dv = torch.empty_like(v)
+    ws = torch.empty(api.workspace_size(desc, H, hd, q.dtype, api.ZL_OP_BWD), dtype=torch.uint8, device=dev)
+
+    def step():
+        api.attn_fwd(desc, q, k, v, w.scale, out, lse, o_part, lse_part)
+        if w.num_slots:
+            api.lse_merge(desc, o_part, lse_part, out, lse)
+        api.attn_bwd(desc, q, k, v, out, lse, do, w.scale, dq, dk, dv, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    api.profile_reset()
+    api.profile_enable(True)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    api.profile_enable(False)
+    ms = start.elapsed_time(end) / args.steps
+    kt = {name: api.profile_read(kid) for kid, name in api.KERNEL_NAMES.items()}
+    avg = {name: (t / n if n else 0.0) for name, (t, n) in kt.items()}
+
+    pairs = w.pair_count()
+    fa_flops = 14.0 * hd * H * pairs
+    value = fa_flops / (ms * 1e-3) / 1e12
+    bwd_alg = 8.0 * hd * H * pairs
+    achieved = bwd_alg / (avg["bwd_main"] * 1e-3) / 1e12 if avg["bwd_main"] else 0.0
+    rec = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "heads": H, "head_dim": hd, "total_q": w.total_q, "total_k": w.total_k,
+                   "pairs_per_head": pairs, "shard_rows": w.shard_rows(), "num_slots": w.num_slots},
+        "pct_of_mfma_peak": round(100.0 * value / BF16_PEAK_TFLOPS, 2),
+        "algorithmic_tflops_12d": round(12.0 * hd * H * pairs / (ms * 1e-3) / 1e12, 2),
+        "kernel_ms": {n: round(a, 4) for n, a in avg.items()},
+        "roofline": {"bound": "mfma", "kernel": "bwd_main", "achieved": round(achieved, 2),
+                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
+                     "traffic": None},
+    }
+    if avg["fwd"]:
+        fwd_t = 4.0 * hd * H * pairs / (avg["fwd"] * 1e-3) / 1e12
+        rec["fwd_kernel"] = {"tflops": round(fwd_t, 2), "frac": round(fwd_t / BF16_PEAK_TFLOPS, 4)}
+    if w.num_slots and avg["merge"]:
+        sr = w.shard_rows()
+        nb = max(w.kv_count[s] for s in range(w.num_segments) if w.kind[s] == W.SHARD)
+        mbytes = H * sr * (nb * (4 * hd + 4) + 2 * hd + 4)
+        gbs = mbytes / (avg["merge"] * 1e-3) / 1e9
+        rec["merge_kernel"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                               "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": mbytes}
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_heads)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

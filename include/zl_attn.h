@@ -1,0 +1,197 @@
+/*
+ * zl_attn.h -- C ABI of the packed whole+shard attention library (gfx950).
+ *
+ * One launch computes exact, non-causal softmax attention over a packed batch
+ * that mixes WHOLE segments (a sequence kept whole: configuration (1,1,1),
+ * Sec. IV-A of arXiv 2608.01150) with SHARD segments (a rank's local query
+ * chunk of a context-parallel sequence attending to K/V blocks, the ring axis
+ * of Tab. II).  This is the local compute of the paper's Coalesced Attention
+ * Engine (Sec. IV-D): whole sequences on a rank run as one block-diagonal
+ * call that never mixes attention across sequences and returns outputs in the
+ * rank-local input order; ring-style shards return per-block partial outputs
+ * that are accumulated into the exact result (Sec. II-B).
+ *
+ * Conventions shared by every entry point
+ *   - Packed tensors are contiguous THD row-major: element (t, h, c) of a
+ *     [T, H, d] tensor sits at ((t * H) + h) * d + c.  Q, O, dO, dQ have Tq =
+ *     cu_seqlens_q[num_q_segs] rows; K, V, dK, dV have Tk =
+ *     cu_seqlens_k[num_kv_ranges] rows.  LSE tensors are [T, H] fp32.
+ *   - Partial buffers: o_part [num_slots, Tq, H, d] fp32 and lse_part
+ *     [num_slots, Tq, H] fp32; slot b of a shard row holds the block-locally
+ *     normalised output O_b = softmax_b(S) V_b and its LSE_b.
+ *   - LSE is the natural-log log-sum-exp of the scaled scores.
+ *   - Device pointers are caller-owned (the library never frees or retains
+ *     them); tensor pointers must be 16-byte aligned, LSE pointers 4-byte.
+ *   - Descriptor arrays are HOST memory, read during the call only.
+ *   - `stream` is a hipStream_t (NULL: the null stream).  Work is enqueued
+ *     asynchronously; a call returns once it is enqueued.
+ *   - Every argument is validated before anything is enqueued: an error
+ *     status means no device work was issued and no buffer was touched.
+ *     zl_last_error() then describes the problem.  No C++ exception crosses
+ *     this boundary.
+ *   - The library owns one cache of device work tables (the schedule of a
+ *     descriptor), created on the first call with a new descriptor, reused
+ *     afterwards and released by zl_shutdown().  It allocates no other
+ *     device memory.
+ */
+#ifndef ZL_ATTN_H
+#define ZL_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ZL_ABI_VERSION 1
+
+typedef enum {
+  ZL_OK = 0,
+  ZL_ERR_INVALID_ARG = 1, /* malformed descriptor, pointer, size or scale */
+  ZL_ERR_UNSUPPORTED = 2, /* valid request this build does not implement  */
+  ZL_ERR_WORKSPACE = 3,   /* workspace missing or too small               */
+  ZL_ERR_HIP = 4          /* the HIP runtime reported an error            */
+} zl_status;
+
+/* Segment kinds (Sec. IV-A: (1,1,1) keeps a sequence whole; a split
+ * sequence's local query chunk is a shard). */
+enum { ZL_WHOLE = 0, ZL_SHARD = 1 };
+
+typedef enum { ZL_BF16 = 0, ZL_FP32 = 1 } zl_dtype;
+
+enum { ZL_OP_FWD = 0, ZL_OP_BWD = 1 };
+
+/*
+ * A rank-local schedule of segments (Sec. IV-D: the placement lowered to the
+ * tokens this rank materialises from the sequences' global token ranges).
+ *
+ * Query segment s owns packed query rows [cu_seqlens_q[s], cu_seqlens_q[s+1])
+ * and attends to the K/V ranges kv_first[s] .. kv_first[s]+kv_count[s]-1.
+ * K/V range j owns packed K/V rows [cu_seqlens_k[j], cu_seqlens_k[j+1]).
+ *   WHOLE: kv_count == 1 and the range has exactly as many rows as the
+ *          segment (queries and keys are the same tokens).  Output: final O
+ *          and LSE in `out` / `lse`.
+ *   SHARD: each listed range is one CP block; block_index[j] is its slot in
+ *          the partial buffers (distinct within a segment, < num_slots).  An
+ *          empty range yields O_b = 0, LSE_b = -inf.
+ * q_offset / k_offset give the global token index of the first row of each
+ * segment / range.  They change no value (attention is non-causal, Sec. II-A)
+ * and may be NULL; when given they are checked: non-negative, a WHOLE
+ * segment's q_offset equals its range's k_offset, and the blocks of one
+ * SHARD cover disjoint global token ranges (overlapping blocks would count
+ * keys twice and break exactness).
+ * Forward and merge allow several shards to share a K/V range; backward
+ * requires every range to be used by at most one segment (single owner of
+ * each dK/dV row).
+ */
+typedef struct zl_seg_desc {
+  int32_t num_q_segs;
+  const int32_t* cu_seqlens_q; /* [num_q_segs + 1], starts at 0, non-decreasing */
+  const uint8_t* kind;         /* [num_q_segs] ZL_WHOLE or ZL_SHARD               */
+  const int64_t* q_offset;     /* [num_q_segs] or NULL                           */
+  const int32_t* kv_first;     /* [num_q_segs]                                   */
+  const int32_t* kv_count;     /* [num_q_segs] 1 for WHOLE, >= 1 for SHARD       */
+  int32_t num_kv_ranges;
+  const int32_t* cu_seqlens_k; /* [num_kv_ranges + 1], starts at 0, non-decreasing */
+  const int64_t* k_offset;     /* [num_kv_ranges] or NULL                        */
+  const int32_t* block_index;  /* [num_kv_ranges] CP block id = partial slot      */
+  int32_t num_slots;           /* partial slots; >= 1 when any SHARD exists       */
+} zl_seg_desc;
+
+/* ABI version this library was built with (ZL_ABI_VERSION). */
+int32_t zl_abi_version(void);
+
+/* Message of the last failed call on this thread ("" if none); valid until
+ * the next zl_* call on this thread. */
+const char* zl_last_error(void);
+
+/* Device workspace in bytes that zl_attn_bwd needs for this batch (op =
+ * ZL_OP_BWD: fp32 dQ accumulator [Tq,H,d] plus fp32 D = rowsum(dO*O) [Tq,H]);
+ * 0 for ZL_OP_FWD.  Validates like the call it sizes. */
+zl_status zl_workspace_size(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim,
+                            zl_dtype dtype, int32_t op, size_t* bytes);
+
+/*
+ * Forward of one coalesced launch (Sec. IV-D; ring per-block step of
+ * Sec. II-B / Tab. II for SHARD rows).  For each head h:
+ *   WHOLE row i: out[i,h,:] = sum_j P_ij v_j, lse[i,h] = LSE_i over its range.
+ *   SHARD row i, block j (slot b = block_index[j]):
+ *     o_part[b,i,h,:] = softmax over block j, lse_part[b,i,h] = LSE over j.
+ * S_ij = softmax_scale * q_i . k_j, no mask other than the block diagonal.
+ * q [Tq,H,d], k/v [Tk,H,d] in `dtype` (ZL_BF16; ZL_FP32 for plumbing runs),
+ * out [Tq,H,d] in `dtype`, lse [Tq,H] fp32.  out/lse may be NULL when there
+ * are no WHOLE rows, o_part/lse_part when there are no SHARD rows.  Rows of
+ * other kinds are not written.  head_dim must be 64 or 128.
+ */
+zl_status zl_attn_fwd(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
+                      float softmax_scale, const void* q, const void* k, const void* v,
+                      void* out, float* lse, float* o_part, float* lse_part, int32_t num_slots,
+                      void* stream);
+
+/*
+ * LSE merge of shard partials into exact attention (the ring's output
+ * accumulation, Sec. II-B).  For every SHARD row i and head h, over the slots
+ * B of its blocks:  M = max_b LSE_b, LSE = M + ln sum_b exp(LSE_b - M),
+ * O = sum_b exp(LSE_b - LSE) O_b; slots with LSE_b = -inf are ignored and a
+ * row with no finite slot gets O = 0, LSE = -inf.  Writes out [Tq,H,d] in
+ * `out_dtype` and lse [Tq,H] for SHARD rows only.
+ */
+zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype out_dtype,
+                       const float* o_part, const float* lse_part, int32_t num_slots,
+                       void* out, float* lse, void* stream);
+
+/*
+ * Backward of the packed batch.  `out` and `lse` are the FINAL outputs (for
+ * SHARD rows: merged over all blocks); dout is dL/dout.  With D_i = dO_i.O_i,
+ * P_ij = exp(S_ij - LSE_i), dS_ij = P_ij (dO_i.v_j - D_i):
+ *   dq_i = scale sum_j dS_ij k_j  (a SHARD row sums over all of its blocks),
+ *   dk_j = scale sum_i dS_ij q_i,  dv_j = sum_i P_ij dO_i
+ * (for a SHARD block: this query chunk's contribution).  All tensors in
+ * `dtype` (ZL_BF16 only) except lse (fp32).  dq is [Tq,H,d]; dk, dv are
+ * [Tk,H,d] and rows of ranges no segment uses are not written.  `flags` must
+ * be 0.  workspace: at least zl_workspace_size(..., ZL_OP_BWD) bytes of device
+ * memory, 256-byte aligned, exclusively used by this call until it completes.
+ */
+zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
+                      float softmax_scale, const void* q, const void* k, const void* v,
+                      const void* out, const float* lse, const void* dout,
+                      void* dq, void* dk, void* dv, uint32_t flags,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Host-only view of the schedule a launch would use (no device work): the
+ * work items of op (ZL_OP_FWD or ZL_OP_BWD) in issue order, 8 int32 each:
+ *   q_start, q_len, k_start, k_len, head, slot (-1 for WHOLE), segment, range.
+ * Forward items are query tiles of one (segment, head, range); backward items
+ * are key tiles of one (segment, head, range) covering all of the segment's
+ * queries.  Order: cost = q_len * k_len descending, ties by (segment, head,
+ * q_start, k_start, range) ascending.  Writes min(n, cap) items to `items`
+ * (may be NULL when cap is 0) and the total count to *n.  *tile_m / *tile_n
+ * (may be NULL) receive the query / key tile sizes of that schedule.
+ */
+zl_status zl_plan_dump(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
+                       int32_t op, int32_t* items, size_t cap, size_t* n,
+                       int32_t* tile_m, int32_t* tile_n);
+
+/*
+ * Per-kernel timing with HIP events (off by default).  While enabled, every
+ * kernel this library launches is bracketed by two events recorded on the
+ * stream it is launched on.  zl_profile_read waits for the pending events of
+ * one kernel family, adds their elapsed times to its totals and returns the
+ * totals since the last reset.  Kernel ids: ZL_K_FWD, ZL_K_MERGE,
+ * ZL_K_BWD_PRE, ZL_K_BWD_MAIN, ZL_K_BWD_FIN.
+ */
+enum { ZL_K_FWD = 0, ZL_K_MERGE = 1, ZL_K_BWD_PRE = 2, ZL_K_BWD_MAIN = 3, ZL_K_BWD_FIN = 4, ZL_K_COUNT = 5 };
+zl_status zl_profile_enable(int32_t on);
+zl_status zl_profile_read(int32_t kernel_id, double* total_ms, int64_t* launches);
+void zl_profile_reset(void);
+
+/* Releases the library's device work-table cache (waits for the device). */
+void zl_shutdown(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ZL_ATTN_H */

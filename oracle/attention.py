@@ -122,7 +122,12 @@ def attend_bwd(q, k, v, do, scale, q_rows=None, k_rows=None):
     dv = np.zeros((kj.size, do.shape[1]), np.float64)
     if lq == 0 or lk == 0:
         return dq, dk, dv
-    o, lse = attend(q, k, v, scale)
+    # O and LSE are row-local: only the rows the requested gradients read
+    # are evaluated (every row when any dK/dV row is requested).
+    need = np.arange(lq) if kj.size else qi
+    o = np.zeros((lq, v.shape[1]), np.float64)
+    lse = np.zeros(lq, np.float64)
+    o[need], lse[need] = attend(q[need], k, v, scale)
     dsum = (do * o).sum(axis=1)  # D_i
 
     # dQ for the selected query rows: needs every key of those rows.

@@ -1,0 +1,255 @@
+"""Thin Python binding of the C ABI in include/zl_attn.h (ctypes).
+
+Argument marshalling only: tensors become raw device pointers, the current
+torch stream becomes the hipStream_t, descriptors become ``zl_seg_desc``.
+Every computation runs in the HIP library; if it is not built, importing this
+module raises.  PyTorch supplies device memory and streams.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libzl_attn.so")
+
+ZL_OK, ZL_ERR_INVALID_ARG, ZL_ERR_UNSUPPORTED, ZL_ERR_WORKSPACE, ZL_ERR_HIP = range(5)
+ZL_WHOLE, ZL_SHARD = 0, 1
+ZL_BF16, ZL_FP32 = 0, 1
+ZL_OP_FWD, ZL_OP_BWD = 0, 1
+
+
+class ZlError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"zl status {status}: {message}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build the HIP library first (python -c "
+                          "'import __graft_entry__ as g; g.build()')")
+    return ctypes.CDLL(LIB_PATH)
+
+
+_lib = _load()
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_u8p = ctypes.POINTER(ctypes.c_uint8)
+_vp = ctypes.c_void_p
+
+
+class _CDesc(ctypes.Structure):
+    _fields_ = [
+        ("num_q_segs", ctypes.c_int32),
+        ("cu_seqlens_q", _i32p),
+        ("kind", _u8p),
+        ("q_offset", _i64p),
+        ("kv_first", _i32p),
+        ("kv_count", _i32p),
+        ("num_kv_ranges", ctypes.c_int32),
+        ("cu_seqlens_k", _i32p),
+        ("k_offset", _i64p),
+        ("block_index", _i32p),
+        ("num_slots", ctypes.c_int32),
+    ]
+
+
+def _sig(name, res, *args):
+    fn = getattr(_lib, name)
+    fn.restype = res
+    fn.argtypes = list(args)
+    return fn
+
+
+_DP = ctypes.POINTER(_CDesc)
+_abi_version = _sig("zl_abi_version", ctypes.c_int32)
+_last_error = _sig("zl_last_error", ctypes.c_char_p)
+_workspace_size = _sig("zl_workspace_size", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int,
+                       ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t))
+_fwd = _sig("zl_attn_fwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
+            _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp)
+_merge = _sig("zl_lse_merge", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, _vp, _vp,
+              ctypes.c_int32, _vp, _vp, _vp)
+_bwd = _sig("zl_attn_bwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
+            _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_uint32, _vp, ctypes.c_size_t, _vp)
+_plan_dump = _sig("zl_plan_dump", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_int32,
+                  _i32p, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t), _i32p, _i32p)
+_shutdown = _sig("zl_shutdown", None)
+_prof_enable = _sig("zl_profile_enable", ctypes.c_int, ctypes.c_int32)
+_prof_read = _sig("zl_profile_read", ctypes.c_int, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+                  ctypes.POINTER(ctypes.c_int64))
+_prof_reset = _sig("zl_profile_reset", None)
+
+ZL_K_FWD, ZL_K_MERGE, ZL_K_BWD_PRE, ZL_K_BWD_MAIN, ZL_K_BWD_FIN = range(5)
+KERNEL_NAMES = {ZL_K_FWD: "fwd", ZL_K_MERGE: "merge", ZL_K_BWD_PRE: "bwd_pre", ZL_K_BWD_MAIN: "bwd_main",
+                ZL_K_BWD_FIN: "bwd_fin"}
+
+
+def profile_enable(on: bool) -> None:
+    _check(_prof_enable(1 if on else 0))
+
+
+def profile_reset() -> None:
+    _prof_reset()
+
+
+def profile_read(kernel_id: int):
+    """(total milliseconds, launches) of one kernel family since the last reset."""
+    ms, n = ctypes.c_double(0), ctypes.c_int64(0)
+    _check(_prof_read(kernel_id, ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
+
+
+def abi_version() -> int:
+    return int(_abi_version())
+
+
+def last_error() -> str:
+    return _last_error().decode()
+
+
+def shutdown() -> None:
+    _shutdown()
+
+
+def _check(st: int) -> None:
+    if st != ZL_OK:
+        raise ZlError(st, last_error())
+
+
+class SegDesc:
+    """Host-side ``zl_seg_desc`` with its arrays kept alive.
+
+    Built from any object with the descriptor fields (a ``Workload``, a dict
+    wrapper) or from keyword arrays.  ``q_offset`` / ``k_offset`` may be None.
+    """
+
+    def __init__(self, cu_seqlens_q, kind, kv_first, kv_count, cu_seqlens_k, block_index, num_slots,
+                 q_offset=None, k_offset=None):
+        self._a = {
+            "cu_seqlens_q": np.ascontiguousarray(cu_seqlens_q, dtype=np.int32),
+            "kind": np.ascontiguousarray(kind, dtype=np.uint8),
+            "kv_first": np.ascontiguousarray(kv_first, dtype=np.int32),
+            "kv_count": np.ascontiguousarray(kv_count, dtype=np.int32),
+            "cu_seqlens_k": np.ascontiguousarray(cu_seqlens_k, dtype=np.int32),
+            "block_index": np.ascontiguousarray(block_index, dtype=np.int32),
+        }
+        if q_offset is not None:
+            self._a["q_offset"] = np.ascontiguousarray(q_offset, dtype=np.int64)
+        if k_offset is not None:
+            self._a["k_offset"] = np.ascontiguousarray(k_offset, dtype=np.int64)
+        a = self._a
+        self.c = _CDesc()
+        self.c.num_q_segs = len(a["kind"])
+        self.c.num_kv_ranges = len(a["cu_seqlens_k"]) - 1
+        self.c.num_slots = int(num_slots)
+        for name, ptype in (("cu_seqlens_q", _i32p), ("kind", _u8p), ("kv_first", _i32p), ("kv_count", _i32p),
+                            ("cu_seqlens_k", _i32p), ("block_index", _i32p), ("q_offset", _i64p),
+                            ("k_offset", _i64p)):
+            arr = a.get(name)
+            setattr(self.c, name, arr.ctypes.data_as(ptype) if arr is not None and arr.size else ptype())
+        self.num_slots = int(num_slots)
+        self.total_q = int(a["cu_seqlens_q"][-1])
+        self.total_k = int(a["cu_seqlens_k"][-1])
+
+    @classmethod
+    def of(cls, w) -> "SegDesc":
+        get = (lambda n: w[n]) if isinstance(w, dict) else (lambda n: getattr(w, n))
+        return cls(get("cu_seqlens_q"), get("kind"), get("kv_first"), get("kv_count"), get("cu_seqlens_k"),
+                   get("block_index"), get("num_slots"), q_offset=get("q_offset"), k_offset=get("k_offset"))
+
+    def ptr(self):
+        return ctypes.byref(self.c)
+
+
+def _dtype_code(t: torch.dtype) -> int:
+    if t == torch.bfloat16:
+        return ZL_BF16
+    if t == torch.float32:
+        return ZL_FP32
+    raise ZlError(ZL_ERR_UNSUPPORTED, f"dtype {t} unsupported")
+
+
+def _p(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ZlError(ZL_ERR_INVALID_ARG, "tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def workspace_size(desc: SegDesc, num_heads: int, head_dim: int, dtype: torch.dtype, op: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_workspace_size(desc.ptr(), num_heads, head_dim, _dtype_code(dtype), op, ctypes.byref(n)))
+    return int(n.value)
+
+
+def plan_dump(desc: SegDesc, num_heads: int, head_dim: int, dtype: torch.dtype, op: int):
+    """Work items of a launch in issue order: int32 [n, 8] and (tile_m, tile_n)."""
+    n = ctypes.c_size_t(0)
+    tm, tn = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(_plan_dump(desc.ptr(), num_heads, head_dim, _dtype_code(dtype), op, None, 0, ctypes.byref(n),
+                      ctypes.byref(tm), ctypes.byref(tn)))
+    items = np.zeros((int(n.value), 8), dtype=np.int32)
+    if items.size:
+        _check(_plan_dump(desc.ptr(), num_heads, head_dim, _dtype_code(dtype), op, items.ctypes.data_as(_i32p),
+                          items.shape[0], ctypes.byref(n), None, None))
+    return items, (tm.value, tn.value)
+
+
+def attn_fwd(desc: SegDesc, q, k, v, scale: float, out=None, lse=None, o_part=None, lse_part=None):
+    """zl_attn_fwd.  Allocates the outputs it is not given; returns (out, lse, o_part, lse_part)."""
+    tq, h, d = q.shape
+    dev = q.device
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((tq, h), dtype=torch.float32, device=dev)
+    if o_part is None and desc.num_slots > 0:
+        o_part = torch.empty((desc.num_slots, tq, h, d), dtype=torch.float32, device=dev)
+    if lse_part is None and desc.num_slots > 0:
+        lse_part = torch.empty((desc.num_slots, tq, h), dtype=torch.float32, device=dev)
+    _check(_fwd(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
+                _p(o_part), _p(lse_part), desc.num_slots, _stream(dev)))
+    return out, lse, o_part, lse_part
+
+
+def lse_merge(desc: SegDesc, o_part, lse_part, out, lse):
+    """zl_lse_merge: writes the SHARD rows of out / lse."""
+    tq, h, d = out.shape
+    _check(_merge(desc.ptr(), h, d, _dtype_code(out.dtype), _p(o_part), _p(lse_part), desc.num_slots, _p(out),
+                  _p(lse), _stream(out.device)))
+    return out, lse
+
+
+def attn_bwd(desc: SegDesc, q, k, v, out, lse, dout, scale: float, dq=None, dk=None, dv=None, workspace=None):
+    """zl_attn_bwd.  Allocates dq/dk/dv/workspace it is not given; returns (dq, dk, dv)."""
+    tq, h, d = q.shape
+    dev = q.device
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.zeros_like(k) if dk is None else dk
+    dv = torch.zeros_like(v) if dv is None else dv
+    if workspace is None:
+        workspace = torch.empty(workspace_size(desc, h, d, q.dtype, ZL_OP_BWD), dtype=torch.uint8, device=dev)
+    _check(_bwd(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
+                _p(dout), _p(dq), _p(dk), _p(dv), 0, _p(workspace), workspace.numel(), _stream(dev)))
+    return dq, dk, dv
+
+
+def header_symbols(header_path: Optional[str] = None) -> Sequence[str]:
+    """Function names declared in include/zl_attn.h."""
+    import re
+    if header_path is None:
+        header_path = os.path.join(os.path.dirname(_PKG), "include", "zl_attn.h")
+    text = open(header_path).read()
+    return sorted(set(re.findall(r"\b(zl_[a-z_]+)\s*\(", text)))

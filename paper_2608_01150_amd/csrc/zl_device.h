@@ -1,0 +1,54 @@
+// Device-side helpers shared by the gfx950 kernels: vector types, the bf16
+// MFMA wrapper, bf16 packing and the LDS swizzles.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace zl {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// D(32x32 fp32) += A(32x16 bf16) * B(16x32 bf16).
+// Lane l supplies row l%32 of A and column l%32 of B, each as the 8 values of
+// k-group l/32.  D register i of lane l is element (row 8*(i/4) + 4*(l/32) +
+// i%4, column l%32).
+__device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                 0, 0, 0);
+}
+
+// Round-to-nearest-even fp32 -> bf16 of two values, packed lo | hi << 16.
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  const __bf16 a = (__bf16)lo, b = (__bf16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Row permutation of a 32-row MFMA operand tile.  Loading A-operand row m
+// with tile row perm32(m) makes D register i of lane l hold tile row
+// 16*(i/8) + 8*(l/32) + i%8: each lane's registers 0-7 and 8-15 cover two runs
+// of 8 consecutive rows, so a D fragment is directly the (lane-major) B
+// operand of the next MFMA over those rows, and epilogue stores are 8-wide.
+__device__ __forceinline__ int perm32(int m) {
+  const int blk4 = m >> 3, g = (m >> 2) & 1, lo = m & 3;
+  return ((blk4 >> 1) << 4) + (g << 3) + ((blk4 & 1) << 2) + lo;
+}
+
+// XOR swizzle of 16-byte chunks within an LDS row, keyed by the row index:
+// the 8 rows perm32 sends to 8 consecutive lanes land on 8 distinct chunks.
+__device__ __forceinline__ int swz(int row) { return (row ^ ((row >> 3) << 2)) & 7; }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+constexpr float kNegBig = -1.0e30f;    // finite "minus infinity" for masked scores
+constexpr float kLn2 = 0.69314718055994531f;
+
+}  // namespace zl

@@ -1,0 +1,574 @@
+// Host side of the C ABI: argument validation, the segment scheduler, the
+// device work-table cache and kernel launches.
+//
+// The scheduler lowers a rank-local segment list (Sec. IV-D of arXiv
+// 2608.01150: the placement materialised as the rank's own token ranges) into
+// work items and orders them longest-processing-time first: cost = rows x keys,
+// the quadratic attention work of Sec. II-A.  Ties follow segment order, the
+// analogue of the engine's "decreasing split degree, ties by placement order"
+// rule.  With the hardware dispatcher handing each free compute unit the next
+// workgroup in this order, the launch runs as greedy list scheduling of the
+// items in LPT order, the same "largest first, to the least-loaded place"
+// rule the paper's Filler Packing (Eq. 8) uses across ranks.
+
+#include "zl_attn.h"
+#include "zl_internal.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <list>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+namespace {
+
+thread_local std::string g_last_error;
+
+zl_status fail(zl_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+zl_status fail(zl_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+zl_status ok() {
+  g_last_error.clear();
+  return ZL_OK;
+}
+
+// Which buffers a validated descriptor touches.
+struct Shape {
+  int64_t total_q = 0, total_k = 0;
+  bool any_whole_rows = false, any_shard_rows = false;
+  bool ranges_single_owner = true;
+};
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_slots, Shape* out) {
+  if (!d) return fail(ZL_ERR_INVALID_ARG, "descriptor is NULL");
+  const int32_t nq = d->num_q_segs, nk = d->num_kv_ranges;
+  if (nq < 0 || nk < 0) return fail(ZL_ERR_INVALID_ARG, "negative segment or range count");
+  if (!d->cu_seqlens_q || !d->cu_seqlens_k)
+    return fail(ZL_ERR_INVALID_ARG, "cu_seqlens_q / cu_seqlens_k must not be NULL");
+  if (nq > 0 && (!d->kind || !d->kv_first || !d->kv_count))
+    return fail(ZL_ERR_INVALID_ARG, "kind / kv_first / kv_count must not be NULL");
+  if (nk > 0 && !d->block_index) return fail(ZL_ERR_INVALID_ARG, "block_index must not be NULL");
+  if (d->cu_seqlens_q[0] != 0) return fail(ZL_ERR_INVALID_ARG, "cu_seqlens_q[0] must be 0");
+  if (d->cu_seqlens_k[0] != 0) return fail(ZL_ERR_INVALID_ARG, "cu_seqlens_k[0] must be 0");
+  for (int32_t s = 0; s < nq; ++s)
+    if (d->cu_seqlens_q[s + 1] < d->cu_seqlens_q[s])
+      return fail(ZL_ERR_INVALID_ARG, "cu_seqlens_q decreases at segment %d", s);
+  for (int32_t j = 0; j < nk; ++j)
+    if (d->cu_seqlens_k[j + 1] < d->cu_seqlens_k[j])
+      return fail(ZL_ERR_INVALID_ARG, "cu_seqlens_k decreases at range %d", j);
+  const int32_t nslots = d->num_slots;
+  if (nslots < 0) return fail(ZL_ERR_INVALID_ARG, "num_slots is negative");
+  if (check_slots && num_slots_arg != nslots)
+    return fail(ZL_ERR_INVALID_ARG, "num_slots argument (%d) differs from the descriptor's (%d)",
+                num_slots_arg, nslots);
+  std::vector<int32_t> owners(nk, 0);
+  Shape sh;
+  sh.total_q = d->cu_seqlens_q[nq];
+  sh.total_k = d->cu_seqlens_k[nk];
+  for (int32_t s = 0; s < nq; ++s) {
+    const int32_t lq = d->cu_seqlens_q[s + 1] - d->cu_seqlens_q[s];
+    const int kind = d->kind[s];
+    const int32_t f = d->kv_first[s], c = d->kv_count[s];
+    if (kind != ZL_WHOLE && kind != ZL_SHARD)
+      return fail(ZL_ERR_INVALID_ARG, "segment %d has unknown kind %d", s, kind);
+    if (c < 1) return fail(ZL_ERR_INVALID_ARG, "segment %d has kv_count %d < 1", s, c);
+    if (f < 0 || f > nk - c)
+      return fail(ZL_ERR_INVALID_ARG, "segment %d uses ranges [%d, %d) outside [0, %d)", s, f, f + c, nk);
+    if (d->q_offset && d->q_offset[s] < 0)
+      return fail(ZL_ERR_INVALID_ARG, "segment %d has a negative q_offset", s);
+    for (int32_t j = f; j < f + c; ++j) owners[j]++;
+    if (kind == ZL_WHOLE) {
+      if (c != 1) return fail(ZL_ERR_INVALID_ARG, "WHOLE segment %d must use exactly one range", s);
+      const int32_t lk = d->cu_seqlens_k[f + 1] - d->cu_seqlens_k[f];
+      if (lk != lq)
+        return fail(ZL_ERR_INVALID_ARG, "WHOLE segment %d has %d queries but range %d has %d keys", s, lq, f, lk);
+      if (d->q_offset && d->k_offset && d->q_offset[s] != d->k_offset[f])
+        return fail(ZL_ERR_INVALID_ARG, "WHOLE segment %d: q_offset differs from its range's k_offset", s);
+      if (lq > 0) sh.any_whole_rows = true;
+    } else {
+      if (lq > 0) sh.any_shard_rows = true;
+      for (int32_t j = f; j < f + c; ++j) {
+        const int32_t b = d->block_index[j];
+        if (b < 0 || b >= nslots)
+          return fail(ZL_ERR_INVALID_ARG, "SHARD segment %d: range %d has block_index %d outside [0, %d)",
+                      s, j, b, nslots);
+        for (int32_t i = f; i < j; ++i)
+          if (d->block_index[i] == b)
+            return fail(ZL_ERR_INVALID_ARG, "SHARD segment %d: ranges %d and %d write the same slot %d",
+                        s, i, j, b);
+        if (d->k_offset) {
+          if (d->k_offset[j] < 0) return fail(ZL_ERR_INVALID_ARG, "range %d has a negative k_offset", j);
+          const int64_t a0 = d->k_offset[j], a1 = a0 + (d->cu_seqlens_k[j + 1] - d->cu_seqlens_k[j]);
+          for (int32_t i = f; i < j; ++i) {
+            const int64_t b0 = d->k_offset[i], b1 = b0 + (d->cu_seqlens_k[i + 1] - d->cu_seqlens_k[i]);
+            if (a0 < b1 && b0 < a1)
+              return fail(ZL_ERR_INVALID_ARG,
+                          "SHARD segment %d: blocks %d and %d overlap in global token positions", s, i, j);
+          }
+        }
+      }
+    }
+  }
+  for (int32_t j = 0; j < nk; ++j)
+    if (owners[j] > 1) sh.ranges_single_owner = false;
+  if (sh.any_shard_rows && nslots < 1) return fail(ZL_ERR_INVALID_ARG, "SHARD rows need num_slots >= 1");
+  *out = sh;
+  return ZL_OK;
+}
+
+zl_status validate_common(int32_t H, int32_t hd, zl_dtype dt, float scale, bool need_scale) {
+  if (H < 1) return fail(ZL_ERR_INVALID_ARG, "num_heads must be >= 1 (got %d)", H);
+  if (hd != 64 && hd != 128) return fail(ZL_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", hd);
+  if (dt != ZL_BF16 && dt != ZL_FP32) return fail(ZL_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (need_scale && !(std::isfinite(scale) && scale > 0.f))
+    return fail(ZL_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
+  return ZL_OK;
+}
+
+zl_status check_sizes(const Shape& sh, int32_t H, int32_t hd, int32_t nslots) {
+  // Row indices are int32 in the work tables; element offsets are int64.
+  const int64_t lim = (int64_t)1 << 31;
+  if (sh.total_q >= lim || sh.total_k >= lim) return fail(ZL_ERR_UNSUPPORTED, "more than 2^31-1 rows");
+  if ((double)nslots * sh.total_q * H * hd > 9.0e18) return fail(ZL_ERR_UNSUPPORTED, "partial buffer too large");
+  return ZL_OK;
+}
+
+// ---------------------------------------------------------------- scheduler
+
+struct TileCfg {
+  int m, n;
+};
+
+TileCfg tile_cfg(zl_dtype dt, int op) {
+  if (op == ZL_OP_FWD) return dt == ZL_BF16 ? TileCfg{zl::kFwdTileM, zl::kFwdTileN}
+                                            : TileCfg{zl::kFwd32TileM, zl::kFwd32TileN};
+  return TileCfg{zl::kBwdTileM, zl::kBwdTileN};
+}
+
+std::vector<zl::Item> build_items(const zl_seg_desc* d, int32_t H, int op, TileCfg t) {
+  std::vector<zl::Item> items;
+  for (int32_t s = 0; s < d->num_q_segs; ++s) {
+    const int32_t q0 = d->cu_seqlens_q[s], q1 = d->cu_seqlens_q[s + 1];
+    if (q1 == q0) continue;
+    const bool shard = d->kind[s] == ZL_SHARD;
+    for (int32_t j = d->kv_first[s]; j < d->kv_first[s] + d->kv_count[s]; ++j) {
+      const int32_t k0 = d->cu_seqlens_k[j], k1 = d->cu_seqlens_k[j + 1];
+      const int32_t slot = shard ? d->block_index[j] : -1;
+      for (int32_t h = 0; h < H; ++h) {
+        if (op == ZL_OP_FWD) {
+          for (int32_t t0 = q0; t0 < q1; t0 += t.m)
+            items.push_back({t0, std::min(t.m, q1 - t0), k0, k1 - k0, h, slot, s, j});
+        } else {
+          for (int32_t t0 = k0; t0 < k1; t0 += t.n)
+            items.push_back({q0, q1 - q0, t0, std::min(t.n, k1 - t0), h, slot, s, j});
+        }
+      }
+    }
+  }
+  std::stable_sort(items.begin(), items.end(), [](const zl::Item& a, const zl::Item& b) {
+    const int64_t ca = (int64_t)a.q_len * a.k_len, cb = (int64_t)b.q_len * b.k_len;
+    if (ca != cb) return ca > cb;
+    if (a.seg != b.seg) return a.seg < b.seg;
+    if (a.head != b.head) return a.head < b.head;
+    if (a.q_start != b.q_start) return a.q_start < b.q_start;
+    if (a.k_start != b.k_start) return a.k_start < b.k_start;
+    return a.range < b.range;
+  });
+  return items;
+}
+
+struct MergeTable {
+  std::vector<zl::MergeSeg> segs;
+  std::vector<int32_t> slots;
+  int64_t units = 0;
+};
+
+MergeTable build_merge(const zl_seg_desc* d, int32_t H) {
+  MergeTable t;
+  for (int32_t s = 0; s < d->num_q_segs; ++s) {
+    if (d->kind[s] != ZL_SHARD) continue;
+    const int32_t q0 = d->cu_seqlens_q[s], lq = d->cu_seqlens_q[s + 1] - q0;
+    if (lq == 0) continue;
+    zl::MergeSeg m{q0, lq, (int32_t)t.slots.size(), d->kv_count[s], t.units};
+    for (int32_t j = d->kv_first[s]; j < d->kv_first[s] + d->kv_count[s]; ++j) t.slots.push_back(d->block_index[j]);
+    t.segs.push_back(m);
+    t.units += (int64_t)lq * H;
+  }
+  return t;
+}
+
+// ------------------------------------------------------------- plan cache
+
+struct Plan {
+  std::vector<int64_t> key;
+  int device = -1;
+  void* dev = nullptr;          // device copy of the table(s)
+  std::vector<char> host;       // host copy (source of the upload)
+  int32_t n_items = 0;
+  int32_t n_segs = 0;
+  int64_t n_units = 0;
+  size_t slots_offset = 0;
+};
+
+std::mutex g_mu;
+std::list<Plan> g_plans;  // most recently used first
+constexpr size_t kMaxPlans = 64;
+
+std::vector<int64_t> plan_key(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int op, int dev) {
+  std::vector<int64_t> k = {op, (int64_t)dt, H, hd, dev, d->num_q_segs, d->num_kv_ranges, d->num_slots};
+  for (int32_t s = 0; s <= d->num_q_segs; ++s) k.push_back(d->cu_seqlens_q[s]);
+  for (int32_t s = 0; s < d->num_q_segs; ++s) {
+    k.push_back(d->kind[s]);
+    k.push_back(d->kv_first[s]);
+    k.push_back(d->kv_count[s]);
+  }
+  for (int32_t j = 0; j <= d->num_kv_ranges; ++j) k.push_back(d->cu_seqlens_k[j]);
+  for (int32_t j = 0; j < d->num_kv_ranges; ++j) k.push_back(d->block_index[j]);
+  return k;
+}
+
+// Returns the cached plan for this descriptor, building and uploading it on a
+// miss.  Caller holds g_mu.
+zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int op, hipStream_t stream,
+                   Plan** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(ZL_ERR_HIP, "hipGetDevice failed: no usable GPU");
+  std::vector<int64_t> key = plan_key(d, H, hd, dt, op, dev);
+  for (auto it = g_plans.begin(); it != g_plans.end(); ++it) {
+    if (it->key == key) {
+      g_plans.splice(g_plans.begin(), g_plans, it);
+      *out = &g_plans.front();
+      return ZL_OK;
+    }
+  }
+  Plan p;
+  p.key = std::move(key);
+  p.device = dev;
+  if (op == 2) {
+    MergeTable t = build_merge(d, H);
+    p.n_segs = (int32_t)t.segs.size();
+    p.n_units = t.units;
+    const size_t seg_bytes = t.segs.size() * sizeof(zl::MergeSeg);
+    p.slots_offset = (seg_bytes + 255) / 256 * 256;
+    p.host.resize(p.slots_offset + t.slots.size() * sizeof(int32_t));
+    if (seg_bytes) std::memcpy(p.host.data(), t.segs.data(), seg_bytes);
+    if (!t.slots.empty()) std::memcpy(p.host.data() + p.slots_offset, t.slots.data(), t.slots.size() * 4);
+  } else {
+    std::vector<zl::Item> items = build_items(d, H, op, tile_cfg(dt, op));
+    if (items.size() > (size_t)INT32_MAX) return fail(ZL_ERR_UNSUPPORTED, "too many work items");
+    p.n_items = (int32_t)items.size();
+    p.host.resize(items.size() * sizeof(zl::Item));
+    if (!items.empty()) std::memcpy(p.host.data(), items.data(), p.host.size());
+  }
+  if (!p.host.empty()) {
+    if (hipMalloc(&p.dev, p.host.size()) != hipSuccess)
+      return fail(ZL_ERR_HIP, "hipMalloc of a %zu-byte work table failed", p.host.size());
+    if (hipMemcpyAsync(p.dev, p.host.data(), p.host.size(), hipMemcpyHostToDevice, stream) != hipSuccess) {
+      (void)hipFree(p.dev);
+      return fail(ZL_ERR_HIP, "upload of the work table failed");
+    }
+  }
+  g_plans.push_front(std::move(p));
+  while (g_plans.size() > kMaxPlans) {
+    Plan& victim = g_plans.back();
+    if (victim.dev) {
+      int cur = 0;
+      (void)hipGetDevice(&cur);
+      (void)hipSetDevice(victim.device);
+      (void)hipDeviceSynchronize();
+      (void)hipFree(victim.dev);
+      (void)hipSetDevice(cur);
+    }
+    g_plans.pop_back();
+  }
+  *out = &g_plans.front();
+  return ZL_OK;
+}
+
+// ------------------------------------------------------------- profiler
+
+struct ProfSlot {
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pending;
+  double total_ms = 0.0;
+  int64_t launches = 0;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+ProfSlot g_prof[ZL_K_COUNT];
+
+// Runs `launch` (which enqueues one kernel on `s`), bracketed by events when
+// profiling is on.
+template <class F>
+hipError_t timed(int kid, hipStream_t s, F&& launch) {
+  bool on;
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    on = g_prof_on;
+  }
+  if (!on) return launch();
+  hipEvent_t a = nullptr, b = nullptr;
+  if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return hipErrorOutOfMemory;
+  (void)hipEventRecord(a, s);
+  const hipError_t e = launch();
+  (void)hipEventRecord(b, s);
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof[kid].pending.emplace_back(a, b);
+  return e;
+}
+
+zl_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(ZL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t zl_abi_version(void) { return ZL_ABI_VERSION; }
+
+const char* zl_last_error(void) { return g_last_error.c_str(); }
+
+zl_status zl_workspace_size(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, int32_t op,
+                            size_t* bytes) {
+  if (!bytes) return fail(ZL_ERR_INVALID_ARG, "bytes is NULL");
+  zl_status st = validate_common(H, hd, dt, 1.f, false);
+  if (st != ZL_OK) return st;
+  Shape sh;
+  if ((st = validate_desc(desc, 0, false, &sh)) != ZL_OK) return st;
+  if (op == ZL_OP_FWD) {
+    *bytes = 0;
+    return ok();
+  }
+  if (op != ZL_OP_BWD) return fail(ZL_ERR_INVALID_ARG, "op must be ZL_OP_FWD or ZL_OP_BWD");
+  const size_t acc = (size_t)sh.total_q * H * hd * sizeof(float);
+  const size_t dsum = (size_t)sh.total_q * H * sizeof(float);
+  *bytes = (acc + 255) / 256 * 256 + (dsum + 255) / 256 * 256;
+  return ok();
+}
+
+zl_status zl_attn_fwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
+                      const void* k, const void* v, void* out, float* lse, float* o_part, float* lse_part,
+                      int32_t num_slots, void* stream) {
+  zl_status st = validate_common(H, hd, dt, scale, true);
+  if (st != ZL_OK) return st;
+  Shape sh;
+  if ((st = validate_desc(desc, num_slots, true, &sh)) != ZL_OK) return st;
+  if ((st = check_sizes(sh, H, hd, num_slots)) != ZL_OK) return st;
+  if (sh.total_q > 0 && !q) return fail(ZL_ERR_INVALID_ARG, "q is NULL");
+  if (sh.total_k > 0 && (!k || !v)) return fail(ZL_ERR_INVALID_ARG, "k or v is NULL");
+  if (sh.any_whole_rows && (!out || !lse)) return fail(ZL_ERR_INVALID_ARG, "WHOLE rows need out and lse");
+  if (sh.any_shard_rows && (!o_part || !lse_part))
+    return fail(ZL_ERR_INVALID_ARG, "SHARD rows need o_part and lse_part");
+  for (const void* p : {q, k, v, (const void*)out, (const void*)o_part})
+    if (p && !aligned(p, 16)) return fail(ZL_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  for (const void* p : {(const void*)lse, (const void*)lse_part})
+    if (p && !aligned(p, 4)) return fail(ZL_ERR_INVALID_ARG, "LSE pointers must be 4-byte aligned");
+  std::lock_guard<std::mutex> lock(g_mu);
+  Plan* plan = nullptr;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = get_plan(desc, H, hd, dt, ZL_OP_FWD, s, &plan)) != ZL_OK) return st;
+  if (plan->n_items == 0) return ok();
+  zl::FwdParams p{};
+  p.q = q;
+  p.k = k;
+  p.v = v;
+  p.out = out;
+  p.lse = lse;
+  p.o_part = o_part;
+  p.lse_part = lse_part;
+  p.items = static_cast<const zl::Item*>(plan->dev);
+  p.n_items = plan->n_items;
+  p.num_heads = H;
+  p.slot_stride = (int64_t)sh.total_q * H * hd;
+  p.lse_slot_stride = (int64_t)sh.total_q * H;
+  p.scale = scale;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  p.xcd_chunk = 1;
+  hipError_t e = timed(ZL_K_FWD, s, [&] {
+    return dt == ZL_BF16 ? zl::launch_fwd_bf16(p, hd, s) : zl::launch_fwd_fp32(p, hd, s);
+  });
+  return hip_status(e, "forward launch");
+}
+
+zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype out_dt, const float* o_part,
+                       const float* lse_part, int32_t num_slots, void* out, float* lse, void* stream) {
+  zl_status st = validate_common(H, hd, out_dt, 1.f, false);
+  if (st != ZL_OK) return st;
+  Shape sh;
+  if ((st = validate_desc(desc, num_slots, true, &sh)) != ZL_OK) return st;
+  if ((st = check_sizes(sh, H, hd, num_slots)) != ZL_OK) return st;
+  if (!sh.any_shard_rows) return ok();
+  if (!o_part || !lse_part || !out || !lse) return fail(ZL_ERR_INVALID_ARG, "merge needs o_part, lse_part, out, lse");
+  if (!aligned(o_part, 16) || !aligned(out, 16)) return fail(ZL_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  if (!aligned(lse_part, 4) || !aligned(lse, 4)) return fail(ZL_ERR_INVALID_ARG, "LSE pointers must be 4-byte aligned");
+  std::lock_guard<std::mutex> lock(g_mu);
+  Plan* plan = nullptr;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = get_plan(desc, H, hd, out_dt, 2, s, &plan)) != ZL_OK) return st;
+  if (plan->n_units == 0) return ok();
+  zl::MergeParams p{};
+  p.o_part = o_part;
+  p.lse_part = lse_part;
+  p.out = out;
+  p.lse = lse;
+  p.segs = static_cast<const zl::MergeSeg*>(plan->dev);
+  p.slots = reinterpret_cast<const int32_t*>(static_cast<const char*>(plan->dev) + plan->slots_offset);
+  p.n_segs = plan->n_segs;
+  p.num_heads = H;
+  p.n_units = plan->n_units;
+  p.slot_stride = (int64_t)sh.total_q * H * hd;
+  p.lse_slot_stride = (int64_t)sh.total_q * H;
+  return hip_status(timed(ZL_K_MERGE, s, [&] { return zl::launch_merge(p, hd, out_dt == ZL_BF16, s); }),
+                    "merge launch");
+}
+
+zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
+                      const void* k, const void* v, const void* out, const float* lse, const void* dout, void* dq,
+                      void* dk, void* dv, uint32_t flags, void* workspace, size_t ws_bytes, void* stream) {
+  zl_status st = validate_common(H, hd, dt, scale, true);
+  if (st != ZL_OK) return st;
+  if (dt != ZL_BF16) return fail(ZL_ERR_UNSUPPORTED, "backward supports ZL_BF16 only");
+  if (flags != 0) return fail(ZL_ERR_INVALID_ARG, "flags must be 0");
+  Shape sh;
+  if ((st = validate_desc(desc, 0, false, &sh)) != ZL_OK) return st;
+  if ((st = check_sizes(sh, H, hd, 0)) != ZL_OK) return st;
+  if (!sh.ranges_single_owner)
+    return fail(ZL_ERR_INVALID_ARG, "backward needs every K/V range used by at most one segment");
+  if (sh.total_q > 0 && (!q || !out || !lse || !dout || !dq))
+    return fail(ZL_ERR_INVALID_ARG, "q, out, lse, dout and dq must not be NULL");
+  if (sh.total_k > 0 && (!k || !v || !dk || !dv)) return fail(ZL_ERR_INVALID_ARG, "k, v, dk and dv must not be NULL");
+  for (const void* p : {q, k, v, out, dout, (const void*)dq, (const void*)dk, (const void*)dv})
+    if (p && !aligned(p, 16)) return fail(ZL_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  if (lse && !aligned(lse, 4)) return fail(ZL_ERR_INVALID_ARG, "lse must be 4-byte aligned");
+  size_t need = 0;
+  if ((st = zl_workspace_size(desc, H, hd, dt, ZL_OP_BWD, &need)) != ZL_OK) return st;
+  if (need > 0 && (!workspace || ws_bytes < need))
+    return fail(ZL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace ? ws_bytes : 0);
+  if (workspace && !aligned(workspace, 256)) return fail(ZL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (sh.total_q == 0) return ok();
+  std::lock_guard<std::mutex> lock(g_mu);
+  Plan* plan = nullptr;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = get_plan(desc, H, hd, dt, ZL_OP_BWD, s, &plan)) != ZL_OK) return st;
+  zl::BwdParams p{};
+  p.q = q;
+  p.k = k;
+  p.v = v;
+  p.out = out;
+  p.lse = lse;
+  p.dout = dout;
+  p.dq = dq;
+  p.dk = dk;
+  p.dv = dv;
+  const size_t acc = (size_t)sh.total_q * H * hd * sizeof(float);
+  p.dq_acc = static_cast<float*>(workspace);
+  p.dsum = reinterpret_cast<float*>(static_cast<char*>(workspace) + (acc + 255) / 256 * 256);
+  p.items = static_cast<const zl::Item*>(plan->dev);
+  p.n_items = plan->n_items;
+  p.num_heads = H;
+  p.total_q = sh.total_q;
+  p.scale = scale;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  p.xcd_chunk = 1;
+  hipError_t e = timed(ZL_K_BWD_PRE, s, [&] { return zl::launch_bwd_bf16(p, hd, 0, s); });
+  if (e == hipSuccess) e = timed(ZL_K_BWD_MAIN, s, [&] { return zl::launch_bwd_bf16(p, hd, 1, s); });
+  if (e == hipSuccess) e = timed(ZL_K_BWD_FIN, s, [&] { return zl::launch_bwd_bf16(p, hd, 2, s); });
+  return hip_status(e, "backward launch");
+}
+
+zl_status zl_plan_dump(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, int32_t op, int32_t* items,
+                       size_t cap, size_t* n, int32_t* tile_m, int32_t* tile_n) {
+  zl_status st = validate_common(H, hd, dt, 1.f, false);
+  if (st != ZL_OK) return st;
+  if (op != ZL_OP_FWD && op != ZL_OP_BWD) return fail(ZL_ERR_INVALID_ARG, "op must be ZL_OP_FWD or ZL_OP_BWD");
+  if (!n) return fail(ZL_ERR_INVALID_ARG, "n is NULL");
+  if (cap > 0 && !items) return fail(ZL_ERR_INVALID_ARG, "items is NULL with cap > 0");
+  Shape sh;
+  if ((st = validate_desc(desc, 0, false, &sh)) != ZL_OK) return st;
+  const TileCfg t = tile_cfg(dt, op);
+  std::vector<zl::Item> v = build_items(desc, H, op, t);
+  *n = v.size();
+  const size_t m = std::min(cap, v.size());
+  if (m) std::memcpy(items, v.data(), m * sizeof(zl::Item));
+  if (tile_m) *tile_m = t.m;
+  if (tile_n) *tile_n = t.n;
+  return ok();
+}
+
+zl_status zl_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_on = on != 0;
+  return ok();
+}
+
+zl_status zl_profile_read(int32_t kid, double* total_ms, int64_t* launches) {
+  if (kid < 0 || kid >= ZL_K_COUNT) return fail(ZL_ERR_INVALID_ARG, "unknown kernel id %d", kid);
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    ev.swap(g_prof[kid].pending);
+  }
+  double add = 0.0;
+  hipError_t err = hipSuccess;
+  for (auto& pr : ev) {
+    float ms = 0.f;
+    if (err == hipSuccess) err = hipEventSynchronize(pr.second);
+    if (err == hipSuccess) err = hipEventElapsedTime(&ms, pr.first, pr.second);
+    add += ms;
+    (void)hipEventDestroy(pr.first);
+    (void)hipEventDestroy(pr.second);
+  }
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof[kid].total_ms += add;
+  g_prof[kid].launches += (int64_t)ev.size();
+  if (total_ms) *total_ms = g_prof[kid].total_ms;
+  if (launches) *launches = g_prof[kid].launches;
+  if (err != hipSuccess) return fail(ZL_ERR_HIP, "event timing failed: %s", hipGetErrorString(err));
+  return ok();
+}
+
+void zl_profile_reset(void) {
+  for (int k = 0; k < ZL_K_COUNT; ++k) {
+    double t;
+    int64_t n;
+    (void)zl_profile_read(k, &t, &n);
+  }
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto& sl : g_prof) {
+    sl.total_ms = 0.0;
+    sl.launches = 0;
+  }
+}
+
+void zl_shutdown(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  int cur = 0;
+  const bool have_dev = hipGetDevice(&cur) == hipSuccess;
+  for (Plan& p : g_plans) {
+    if (p.dev) {
+      (void)hipSetDevice(p.device);
+      (void)hipDeviceSynchronize();
+      (void)hipFree(p.dev);
+    }
+  }
+  g_plans.clear();
+  if (have_dev) (void)hipSetDevice(cur);
+}
+
+}  // extern "C"

@@ -1,0 +1,108 @@
+// Internal interface between the host library (validation, scheduling, plan
+// cache) and the gfx950 kernels.  Not part of the C ABI.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+#include <hip/hip_runtime_api.h>
+
+namespace zl {
+
+// One unit of work of a launch.  Forward: query rows [q_start, q_start+q_len)
+// of one head against the keys [k_start, k_start+k_len) of one K/V range.
+// Backward: keys [k_start, k_start+k_len) of one range against all of the
+// owning segment's queries [q_start, q_start+q_len).
+struct Item {
+  int32_t q_start, q_len, k_start, k_len, head, slot, seg, range;
+};
+static_assert(sizeof(Item) == 32, "work item must stay 32 bytes");
+
+// Tile shapes of each kernel family (rows of Q per forward item, keys per
+// backward item, and the inner tile of the loop each one runs).
+constexpr int kFwdTileM = 128;       // bf16 forward: 4 waves x 32 query rows
+constexpr int kFwdTileN = 64;        // keys per inner step
+constexpr int kFwd32TileM = 64;      // fp32 forward: one query row per lane
+constexpr int kFwd32TileN = 32;
+constexpr int kBwdTileN = 128;       // bf16 backward: 4 waves x 32 keys
+constexpr int kBwdTileM = 32;        // queries per inner step
+
+// Work-item index of workgroup `b`.  Workgroups are dispatched round-robin
+// over the 8 XCDs (b % 8); each run of 8*chunk consecutive workgroups is
+// regrouped so that one XCD takes `chunk` consecutive items (neighbouring
+// query tiles of one head share K/V tiles in that XCD's L2).  A trailing
+// incomplete run keeps the identity order.  A bijection on [0, n).
+__host__ __device__ inline int32_t dispatch_item(int32_t b, int32_t n, int32_t chunk) {
+  const int32_t group = 8 * chunk;
+  if (chunk <= 1) return b;
+  const int32_t base = (b / group) * group;
+  if (base + group > n) return b;
+  const int32_t r = b - base;
+  return base + (r % 8) * chunk + (r / 8);
+}
+
+struct FwdParams {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* out;
+  float* lse;
+  float* o_part;
+  float* lse_part;
+  const Item* items;
+  int32_t n_items;
+  int32_t num_heads;
+  int64_t slot_stride;   // elements between partial slots of o_part (Tq*H*d)
+  int64_t lse_slot_stride;  // Tq*H
+  float scale;           // softmax scale
+  float scale_log2;      // softmax scale * log2(e)
+  int32_t xcd_chunk;
+};
+
+struct MergeSeg {
+  int32_t row_start, row_count, slot_first, slot_count;
+  int64_t unit_start;    // first (row, head) unit of this segment in the flat unit space
+};
+
+struct MergeParams {
+  const float* o_part;
+  const float* lse_part;
+  void* out;
+  float* lse;
+  const MergeSeg* segs;
+  const int32_t* slots;
+  int32_t n_segs;
+  int32_t num_heads;
+  int64_t n_units;
+  int64_t slot_stride;
+  int64_t lse_slot_stride;
+};
+
+struct BwdParams {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* out;
+  const float* lse;
+  const void* dout;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* dq_acc;     // [Tq, H, d] fp32 workspace
+  float* dsum;       // [Tq, H] fp32 workspace: D = rowsum(dO * O)
+  const Item* items;
+  int32_t n_items;
+  int32_t num_heads;
+  int64_t total_q;   // Tq
+  float scale;
+  float scale_log2;
+  int32_t xcd_chunk;
+};
+
+hipError_t launch_fwd_bf16(const FwdParams& p, int head_dim, hipStream_t s);
+hipError_t launch_fwd_fp32(const FwdParams& p, int head_dim, hipStream_t s);
+hipError_t launch_merge(const MergeParams& p, int head_dim, bool out_bf16, hipStream_t s);
+// stage 0: preprocess, 1: main, 2: dQ finalize
+hipError_t launch_bwd_bf16(const BwdParams& p, int head_dim, int stage, hipStream_t s);
+
+}  // namespace zl

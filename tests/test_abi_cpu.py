@@ -1,0 +1,100 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and
+rejects malformed requests before touching any device state."""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_01150_amd import api
+from tests import _descs
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+def test_exports_every_declared_symbol():
+    names = api.header_symbols()
+    assert {"zl_attn_fwd", "zl_attn_bwd", "zl_lse_merge", "zl_plan_dump", "zl_workspace_size",
+            "zl_last_error", "zl_abi_version", "zl_shutdown"} <= set(names)
+    for n in names:
+        assert hasattr(api._lib, n), n
+
+
+def test_abi_version():
+    assert api.abi_version() == 1
+
+
+def _fwd(d, H=2, hd=64, dt=api.ZL_BF16, scale=0.125, nslots=None, ptrs=(FAKE,) * 7):
+    return api._fwd(d.ptr(), H, hd, dt, scale, *ptrs, d.num_slots if nslots is None else nslots, None)
+
+
+def _ok_desc(**over):
+    base = _descs.mixed_small()
+    base.update(over)
+    return api.SegDesc.of(base)
+
+
+@pytest.mark.parametrize("over,needle", [
+    (dict(cu_seqlens_q=(1, 200, 200, 277, 427, 460)), "cu_seqlens_q[0]"),
+    (dict(cu_seqlens_q=(0, 200, 190, 277, 427, 460)), "decreases"),
+    (dict(cu_seqlens_k=(0, 200, 200, 276, 577, 577, 706, 770)), "WHOLE segment 2"),
+    (dict(kind=(0, 0, 0, 1, 2)), "unknown kind"),
+    (dict(kv_count=(1, 1, 1, 0, 1)), "kv_count"),
+    (dict(kv_count=(1, 1, 2, 3, 1)), "exactly one range"),
+    (dict(kv_first=(0, 1, 2, 3, 7)), "outside"),
+    (dict(block_index=(0, 0, 0, 2, 0, 3, 0)), "block_index 3"),
+    (dict(block_index=(0, 0, 0, 2, 2, 1, 0)), "same slot"),
+    (dict(k_offset=(0, 0, 0, 0, 250, 300, 500)), "overlap"),
+    (dict(q_offset=(0, 0, 5, 0, 500)), "q_offset differs"),
+    (dict(q_offset=(0, 0, 0, -1, 500)), "negative q_offset"),
+])
+def test_invalid_descriptors_are_rejected(over, needle):
+    d = _ok_desc(**over)
+    assert _fwd(d) == api.ZL_ERR_INVALID_ARG
+    assert needle in api.last_error()
+
+
+def test_invalid_scalars_and_pointers():
+    d = _ok_desc()
+    assert _fwd(d, H=0) == api.ZL_ERR_INVALID_ARG
+    assert _fwd(d, hd=96) == api.ZL_ERR_UNSUPPORTED
+    assert _fwd(d, scale=0.0) == api.ZL_ERR_INVALID_ARG
+    assert _fwd(d, scale=float("nan")) == api.ZL_ERR_INVALID_ARG
+    assert _fwd(d, dt=7) == api.ZL_ERR_INVALID_ARG
+    assert _fwd(d, nslots=2) == api.ZL_ERR_INVALID_ARG
+    assert _fwd(d, ptrs=(FAKE + 8,) + (FAKE,) * 6) == api.ZL_ERR_INVALID_ARG   # misaligned q
+    assert "16-byte" in api.last_error()
+    assert _fwd(d, ptrs=(FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE)) == api.ZL_ERR_INVALID_ARG  # no out
+    assert _fwd(d, ptrs=(FAKE,) * 5 + (None, FAKE)) == api.ZL_ERR_INVALID_ARG  # no o_part
+    assert api._fwd(None, 2, 64, 0, 0.1, *((FAKE,) * 7), 3, None) == api.ZL_ERR_INVALID_ARG
+
+
+def test_backward_rules():
+    d = _ok_desc()
+    args = [FAKE] * 9
+    # fp32 backward is not built
+    st = api._bwd(d.ptr(), 2, 64, api.ZL_FP32, 0.1, *args, 0, FAKE, 1 << 40, None)
+    assert st == api.ZL_ERR_UNSUPPORTED
+    # unknown flags
+    assert api._bwd(d.ptr(), 2, 64, api.ZL_BF16, 0.1, *args, 1, FAKE, 1 << 40, None) == api.ZL_ERR_INVALID_ARG
+    # workspace too small
+    need = api.workspace_size(d, 2, 64, torch.bfloat16, api.ZL_OP_BWD)
+    assert need == (460 * 2 * 64 * 4 + 255) // 256 * 256 + (460 * 2 * 4 + 255) // 256 * 256
+    st = api._bwd(d.ptr(), 2, 64, api.ZL_BF16, 0.1, *args, 0, FAKE, need - 1, None)
+    assert st == api.ZL_ERR_WORKSPACE
+    # shared K/V ranges are forward-only
+    shared = api.SegDesc.of(_descs.desc((0, 4, 8), (1, 1), (0, 0), (2, 2), (0, 4, 8), (0, 1), 2))
+    st = api._bwd(shared.ptr(), 2, 64, api.ZL_BF16, 0.1, *args, 0, FAKE, 1 << 40, None)
+    assert st == api.ZL_ERR_INVALID_ARG and "at most one segment" in api.last_error()
+
+
+def test_workspace_size_forward_is_zero():
+    assert api.workspace_size(_ok_desc(), 3, 128, torch.bfloat16, api.ZL_OP_FWD) == 0
+
+
+def test_last_error_cleared_by_success():
+    d = _ok_desc()
+    _fwd(d, H=0)
+    assert api.last_error()
+    api.workspace_size(d, 2, 64, torch.bfloat16, api.ZL_OP_FWD)
+    assert api.last_error() == ""
