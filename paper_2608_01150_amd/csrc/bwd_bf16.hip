@@ -233,21 +233,24 @@ __global__ __launch_bounds__(NT, 1) void bwd_main_kernel(BwdParams p) {
     }
     __syncthreads();  // dS of every wave is in LDS
 
-    // dQ^T[d, q] = sum_key K^T[d, key] dS^T[key, q] for this wave's d-block and key part.
+    // dQ[q, d] = sum_key dS[q, key] K[key, d] for this wave's d-block and key part.
+    // A = dS rows (query m = lane%32) from LDS, B = K^T rows (d) from LDS, so a
+    // D register holds one query row and the 32 lanes of a half-wave hold 32
+    // consecutive d: every atomic instruction covers two 128-byte row pieces.
     f32x16 dq = f32x16{};
-    const int drow = dq_db * 32 + perm32(ln);
+    const int dcol = dq_db * 32 + ln;
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
       const int kc = dq_kpart * KSTEPS * 2 + 2 * ks + g;  // 8-key chunk index
-      const u32x4 a = *reinterpret_cast<const u32x4*>(sm.kt + kt_off(drow, kc));
-      const u32x4 b = *reinterpret_cast<const u32x4*>(sm.ds + ds_off(ln, kc));
+      const u32x4 a = *reinterpret_cast<const u32x4*>(sm.ds + ds_off(ln, kc));
+      const u32x4 b = *reinterpret_cast<const u32x4*>(sm.kt + kt_off(dcol, kc));
       dq = mfma32(a, b, dq);
     }
-    // dq[i] is (d = dq_db*32 + 16*(i/8) + 8g + i%8, query ln).
-    if (ln < nq) {
-      float* dst = dqg + (int64_t)(q0 + ln) * rs + dq_db * 32 + 8 * g;
+    // dq[i] is (query 8*(i/4) + 4*g + i%4, d = dcol).
 #pragma unroll
-      for (int i = 0; i < 16; ++i) unsafeAtomicAdd(dst + 16 * (i >> 3) + (i & 7), dq[i]);
+    for (int i = 0; i < 16; ++i) {
+      const int qq = 8 * (i >> 2) + 4 * g + (i & 3);
+      if (qq < nq) unsafeAtomicAdd(dqg + (int64_t)(q0 + qq) * rs + dcol, dq[i]);
     }
   }
 

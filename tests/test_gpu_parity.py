@@ -170,8 +170,6 @@ def test_constant_v_returns_that_row():
     api.lse_merge(desc, o_part, lse_part, out, lse)
     torch.cuda.synchronize()
     expect = row.float().cuda().expand_as(out)
-    live = torch.ones(out.shape[0], dtype=torch.bool)
-    live[200:200] = False
     assert (out.float() - expect).abs().max().item() <= 1e-2
 
 
@@ -185,15 +183,22 @@ def test_segment_isolation_and_determinism():
     a = api.attn_fwd(desc, q.cuda(), k.cuda(), v.cuda(), 0.1)
     b = api.attn_fwd(desc, q.cuda(), k.cuda(), v.cuda(), 0.1)
     torch.cuda.synchronize()
-    assert torch.equal(a[0][:200], b[0][:200]) and torch.equal(a[2][:, 277:], b[2][:, 277:])
+    # written regions only: whole rows of out/lse, slots 2,0,1 of rows 277..427, slot 0 of rows 427..460
+    def written(r):
+        return (r[0][:277], r[1][:277], r[2][[2, 0, 1], 277:427], r[3][[2, 0, 1], 277:427],
+                r[2][0, 427:460], r[3][0, 427:460])
+    for x, y in zip(written(a), written(b)):
+        assert torch.equal(x, y)
     q2, k2, v2 = q.clone(), k.clone(), v.clone()
     q2[200:277] *= -1
     k2[200:277] += 1
     v2[200:277] -= 2
     c = api.attn_fwd(desc, q2.cuda(), k2.cuda(), v2.cuda(), 0.1)
     torch.cuda.synchronize()
-    assert torch.equal(a[0][:200], c[0][:200]) and torch.equal(a[1][:200], c[1][:200])
-    assert torch.equal(a[2][:, 277:], c[2][:, 277:]) and torch.equal(a[3][:, 277:], c[3][:, 277:])
+    wa, wc = written(a), written(c)
+    assert torch.equal(wa[0][:200], wc[0][:200]) and torch.equal(wa[1][:200], wc[1][:200])
+    for x, y in zip(wa[2:], wc[2:]):
+        assert torch.equal(x, y)
     assert not torch.equal(a[0][200:277], c[0][200:277])
 
 
