@@ -60,7 +60,9 @@ enum { ZL_WHOLE = 0, ZL_SHARD = 1 };
 
 typedef enum { ZL_BF16 = 0, ZL_FP32 = 1 } zl_dtype;
 
-enum { ZL_OP_FWD = 0, ZL_OP_BWD = 1 };
+/* Operations.  ZL_OP_BWD_DQ names the second backward schedule (query tiles
+ * that produce dQ) and is accepted by zl_plan_dump only. */
+enum { ZL_OP_FWD = 0, ZL_OP_BWD = 1, ZL_OP_BWD_DQ = 2 };
 
 /*
  * A rank-local schedule of segments (Sec. IV-D: the placement lowered to the
@@ -107,8 +109,8 @@ int32_t zl_abi_version(void);
 const char* zl_last_error(void);
 
 /* Device workspace in bytes that zl_attn_bwd needs for this batch (op =
- * ZL_OP_BWD: fp32 dQ accumulator [Tq,H,d] plus fp32 D = rowsum(dO*O) [Tq,H]);
- * 0 for ZL_OP_FWD.  Validates like the call it sizes. */
+ * ZL_OP_BWD: fp32 D = rowsum(dO*O), [Tq,H]); 0 for ZL_OP_FWD.  Validates
+ * like the call it sizes. */
 zl_status zl_workspace_size(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim,
                             zl_dtype dtype, int32_t op, size_t* bytes);
 
@@ -148,10 +150,11 @@ zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t num_heads, int32_t head_
  *   dq_i = scale sum_j dS_ij k_j  (a SHARD row sums over all of its blocks),
  *   dk_j = scale sum_i dS_ij q_i,  dv_j = sum_i P_ij dO_i
  * (for a SHARD block: this query chunk's contribution).  All tensors in
- * `dtype` (ZL_BF16 only) except lse (fp32).  dq is [Tq,H,d]; dk, dv are
- * [Tk,H,d] and rows of ranges no segment uses are not written.  `flags` must
- * be 0.  workspace: at least zl_workspace_size(..., ZL_OP_BWD) bytes of device
- * memory, 256-byte aligned, exclusively used by this call until it completes.
+ * `dtype` (ZL_BF16 only) except lse (fp32).  dq is [Tq,H,d] and every row of
+ * it is written; dk, dv are [Tk,H,d] and rows of ranges no segment uses are
+ * not written.  No atomics: results are deterministic.  `flags` must be 0.
+ * workspace: at least zl_workspace_size(..., ZL_OP_BWD) bytes of device
+ * memory, 256-byte aligned, used by this call until it completes.
  */
 zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
                       float softmax_scale, const void* q, const void* k, const void* v,
@@ -161,14 +164,19 @@ zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t num_heads, int32_t head_d
 
 /*
  * Host-only view of the schedule a launch would use (no device work): the
- * work items of op (ZL_OP_FWD or ZL_OP_BWD) in issue order, 8 int32 each:
+ * work items of op in issue order, 8 int32 each:
  *   q_start, q_len, k_start, k_len, head, slot (-1 for WHOLE), segment, range.
- * Forward items are query tiles of one (segment, head, range); backward items
- * are key tiles of one (segment, head, range) covering all of the segment's
- * queries.  Order: cost = q_len * k_len descending, ties by (segment, head,
- * q_start, k_start, range) ascending.  Writes min(n, cap) items to `items`
- * (may be NULL when cap is 0) and the total count to *n.  *tile_m / *tile_n
- * (may be NULL) receive the query / key tile sizes of that schedule.
+ *   ZL_OP_FWD     query tiles of one (segment, head, range).
+ *   ZL_OP_BWD     key tiles of one (segment, head, range) against all of the
+ *                 segment's queries (they produce dK, dV).
+ *   ZL_OP_BWD_DQ  query tiles of one (segment, head) against every key of
+ *                 the segment, all of its ranges (they produce dQ); k_start is
+ *                 the first range's first row, k_len the total key count,
+ *                 slot -1, range the first range.
+ * Order: cost = q_len * k_len descending, ties by (segment, head, q_start,
+ * k_start, range) ascending.  Writes min(n, cap) items to `items` (may be
+ * NULL when cap is 0) and the total count to *n.  *tile_m / *tile_n (may be
+ * NULL) receive the query / key tile sizes of that schedule.
  */
 zl_status zl_plan_dump(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
                        int32_t op, int32_t* items, size_t cap, size_t* n,
@@ -180,9 +188,9 @@ zl_status zl_plan_dump(const zl_seg_desc* desc, int32_t num_heads, int32_t head_
  * stream it is launched on.  zl_profile_read waits for the pending events of
  * one kernel family, adds their elapsed times to its totals and returns the
  * totals since the last reset.  Kernel ids: ZL_K_FWD, ZL_K_MERGE,
- * ZL_K_BWD_PRE, ZL_K_BWD_MAIN, ZL_K_BWD_FIN.
+ * ZL_K_BWD_PRE, ZL_K_BWD_DKDV, ZL_K_BWD_DQ.
  */
-enum { ZL_K_FWD = 0, ZL_K_MERGE = 1, ZL_K_BWD_PRE = 2, ZL_K_BWD_MAIN = 3, ZL_K_BWD_FIN = 4, ZL_K_COUNT = 5 };
+enum { ZL_K_FWD = 0, ZL_K_MERGE = 1, ZL_K_BWD_PRE = 2, ZL_K_BWD_DKDV = 3, ZL_K_BWD_DQ = 4, ZL_K_COUNT = 5 };
 zl_status zl_profile_enable(int32_t on);
 zl_status zl_profile_read(int32_t kernel_id, double* total_ms, int64_t* launches);
 void zl_profile_reset(void);

@@ -62,7 +62,11 @@ def row_routing(desc):
 
 
 def work_items(desc, num_heads, op, block_m, block_n):
-    """Canonical, ordered work-item list of one launch (op 0 forward, 1 backward)."""
+    """Canonical, ordered work-item list of one launch.
+
+    op 0: forward; op 1: backward key tiles (dK, dV); op 2: backward query
+    tiles that cover every key of the segment, all of its ranges (dQ).
+    """
     cq = _f(desc, "cu_seqlens_q")
     ck = _f(desc, "cu_seqlens_k")
     kinds = _f(desc, "kind")
@@ -76,6 +80,14 @@ def work_items(desc, num_heads, op, block_m, block_n):
         if lq == 0:
             continue
         shard = int(kinds[s]) == SHARD
+        if op == 2:
+            j0 = int(first[s])
+            j1 = j0 + int(count[s])
+            total = sum(int(ck[j + 1]) - int(ck[j]) for j in range(j0, j1))
+            for h in range(num_heads):
+                for t0 in range(q0, q1, block_m):
+                    items.append((t0, min(block_m, q1 - t0), int(ck[j0]), total, h, -1, s, j0))
+            continue
         for j in range(int(first[s]), int(first[s]) + int(count[s])):
             k0, k1 = int(ck[j]), int(ck[j + 1])
             lk = k1 - k0

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_PKG, "libzl_attn.so")
 ZL_OK, ZL_ERR_INVALID_ARG, ZL_ERR_UNSUPPORTED, ZL_ERR_WORKSPACE, ZL_ERR_HIP = range(5)
 ZL_WHOLE, ZL_SHARD = 0, 1
 ZL_BF16, ZL_FP32 = 0, 1
-ZL_OP_FWD, ZL_OP_BWD = 0, 1
+ZL_OP_FWD, ZL_OP_BWD, ZL_OP_BWD_DQ = 0, 1, 2
 
 
 class ZlError(RuntimeError):
@@ -86,9 +86,9 @@ _prof_read = _sig("zl_profile_read", ctypes.c_int, ctypes.c_int32, ctypes.POINTE
                   ctypes.POINTER(ctypes.c_int64))
 _prof_reset = _sig("zl_profile_reset", None)
 
-ZL_K_FWD, ZL_K_MERGE, ZL_K_BWD_PRE, ZL_K_BWD_MAIN, ZL_K_BWD_FIN = range(5)
-KERNEL_NAMES = {ZL_K_FWD: "fwd", ZL_K_MERGE: "merge", ZL_K_BWD_PRE: "bwd_pre", ZL_K_BWD_MAIN: "bwd_main",
-                ZL_K_BWD_FIN: "bwd_fin"}
+ZL_K_FWD, ZL_K_MERGE, ZL_K_BWD_PRE, ZL_K_BWD_DKDV, ZL_K_BWD_DQ = range(5)
+KERNEL_NAMES = {ZL_K_FWD: "fwd", ZL_K_MERGE: "merge", ZL_K_BWD_PRE: "bwd_pre", ZL_K_BWD_DKDV: "bwd_dkdv",
+                ZL_K_BWD_DQ: "bwd_dq"}
 
 
 def profile_enable(on: bool) -> None:

@@ -45,6 +45,32 @@ __device__ __forceinline__ int perm32(int m) {
 // the 8 rows perm32 sends to 8 consecutive lanes land on 8 distinct chunks.
 __device__ __forceinline__ int swz(int row) { return (row ^ ((row >> 3) << 2)) & 7; }
 
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// LDS transpose read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
+// lane i receives in slot t the 16-bit element (i % 4) of the 8 bytes that
+// lane 4*t + i/4 addresses.
+__device__ __forceinline__ u32x2 lds_read_tr16(const void* p) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
+  return __builtin_bit_cast(u32x2, v);
+}
+
+// MFMA operand whose 8 k-values run down a column of a row-major [k][col]
+// bf16 LDS tile: lane l (m = l%32, g = l/32) receives rows k0 + 8g .. k0 + 8g
+// + 7 of column col_base + perm32(m).  `off(row, col)` is the tile's byte
+// offset of element (row, col); 4 consecutive columns must be 8-byte
+// contiguous.  Two transpose reads, each lane addressing one 8-byte piece of
+// a 4-row x 16-column block.
+template <class Off>
+__device__ __forceinline__ u32x4 tr_operand(const char* tile, int k0, int col_base, int lane, Off off) {
+  const int grp = lane >> 4, i = lane & 15;
+  const int row = k0 + 8 * (lane >> 5) + (i >> 2);
+  const int col = col_base + perm32(16 * (grp & 1) + 4 * (i & 3));
+  const u32x2 lo = lds_read_tr16(tile + off(row, col));
+  const u32x2 hi = lds_read_tr16(tile + off(row + 4, col));
+  return u32x4{lo[0], lo[1], hi[0], hi[1]};
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 

@@ -157,6 +157,7 @@ struct TileCfg {
 TileCfg tile_cfg(zl_dtype dt, int op) {
   if (op == ZL_OP_FWD) return dt == ZL_BF16 ? TileCfg{zl::kFwdTileM, zl::kFwdTileN}
                                             : TileCfg{zl::kFwd32TileM, zl::kFwd32TileN};
+  if (op == ZL_OP_BWD_DQ) return TileCfg{zl::kDqTileM, zl::kDqTileN};
   return TileCfg{zl::kBwdTileM, zl::kBwdTileN};
 }
 
@@ -166,6 +167,15 @@ std::vector<zl::Item> build_items(const zl_seg_desc* d, int32_t H, int op, TileC
     const int32_t q0 = d->cu_seqlens_q[s], q1 = d->cu_seqlens_q[s + 1];
     if (q1 == q0) continue;
     const bool shard = d->kind[s] == ZL_SHARD;
+    if (op == ZL_OP_BWD_DQ) {
+      const int32_t j0 = d->kv_first[s], j1 = j0 + d->kv_count[s];
+      // the segment's ranges are consecutive, so their keys total cu_k[j1] - cu_k[j0]
+      const int32_t total = d->cu_seqlens_k[j1] - d->cu_seqlens_k[j0];
+      for (int32_t h = 0; h < H; ++h)
+        for (int32_t t0 = q0; t0 < q1; t0 += t.m)
+          items.push_back({t0, std::min(t.m, q1 - t0), d->cu_seqlens_k[j0], total, h, -1, s, j0});
+      continue;
+    }
     for (int32_t j = d->kv_first[s]; j < d->kv_first[s] + d->kv_count[s]; ++j) {
       const int32_t k0 = d->cu_seqlens_k[j], k1 = d->cu_seqlens_k[j + 1];
       const int32_t slot = shard ? d->block_index[j] : -1;
@@ -219,11 +229,16 @@ struct Plan {
   int device = -1;
   void* dev = nullptr;          // device copy of the table(s)
   std::vector<char> host;       // host copy (source of the upload)
-  int32_t n_items = 0;
+  int32_t n_items = 0;          // forward items, or backward dK/dV items
+  int32_t n_items2 = 0;         // backward dQ items
   int32_t n_segs = 0;
   int64_t n_units = 0;
-  size_t slots_offset = 0;
+  size_t slots_offset = 0;      // merge: slot list; backward: dQ items
+  size_t cuk_offset = 0;        // backward: cu_seqlens_k copy
+  size_t ranges_offset = 0;     // backward: per-segment ranges
 };
+
+size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
 std::mutex g_mu;
 std::list<Plan> g_plans;  // most recently used first
@@ -268,6 +283,22 @@ zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int
     p.host.resize(p.slots_offset + t.slots.size() * sizeof(int32_t));
     if (seg_bytes) std::memcpy(p.host.data(), t.segs.data(), seg_bytes);
     if (!t.slots.empty()) std::memcpy(p.host.data() + p.slots_offset, t.slots.data(), t.slots.size() * 4);
+  } else if (op == ZL_OP_BWD) {
+    std::vector<zl::Item> kv = build_items(d, H, ZL_OP_BWD, tile_cfg(dt, ZL_OP_BWD));
+    std::vector<zl::Item> qi = build_items(d, H, ZL_OP_BWD_DQ, tile_cfg(dt, ZL_OP_BWD_DQ));
+    if (kv.size() > (size_t)INT32_MAX || qi.size() > (size_t)INT32_MAX)
+      return fail(ZL_ERR_UNSUPPORTED, "too many work items");
+    p.n_items = (int32_t)kv.size();
+    p.n_items2 = (int32_t)qi.size();
+    p.slots_offset = align256(kv.size() * sizeof(zl::Item));
+    p.cuk_offset = p.slots_offset + align256(qi.size() * sizeof(zl::Item));
+    p.ranges_offset = p.cuk_offset + align256((size_t)(d->num_kv_ranges + 1) * sizeof(int32_t));
+    p.host.assign(p.ranges_offset + (size_t)d->num_q_segs * sizeof(zl::SegRanges), 0);
+    if (!kv.empty()) std::memcpy(p.host.data(), kv.data(), kv.size() * sizeof(zl::Item));
+    if (!qi.empty()) std::memcpy(p.host.data() + p.slots_offset, qi.data(), qi.size() * sizeof(zl::Item));
+    std::memcpy(p.host.data() + p.cuk_offset, d->cu_seqlens_k, (size_t)(d->num_kv_ranges + 1) * sizeof(int32_t));
+    zl::SegRanges* sr = reinterpret_cast<zl::SegRanges*>(p.host.data() + p.ranges_offset);
+    for (int32_t s = 0; s < d->num_q_segs; ++s) sr[s] = {d->kv_first[s], d->kv_count[s]};
   } else {
     std::vector<zl::Item> items = build_items(d, H, op, tile_cfg(dt, op));
     if (items.size() > (size_t)INT32_MAX) return fail(ZL_ERR_UNSUPPORTED, "too many work items");
@@ -356,9 +387,7 @@ zl_status zl_workspace_size(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_d
     return ok();
   }
   if (op != ZL_OP_BWD) return fail(ZL_ERR_INVALID_ARG, "op must be ZL_OP_FWD or ZL_OP_BWD");
-  const size_t acc = (size_t)sh.total_q * H * hd * sizeof(float);
-  const size_t dsum = (size_t)sh.total_q * H * sizeof(float);
-  *bytes = (acc + 255) / 256 * 256 + (dsum + 255) / 256 * 256;
+  *bytes = align256((size_t)sh.total_q * H * sizeof(float));
   return ok();
 }
 
@@ -476,19 +505,22 @@ zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype d
   p.dq = dq;
   p.dk = dk;
   p.dv = dv;
-  const size_t acc = (size_t)sh.total_q * H * hd * sizeof(float);
-  p.dq_acc = static_cast<float*>(workspace);
-  p.dsum = reinterpret_cast<float*>(static_cast<char*>(workspace) + (acc + 255) / 256 * 256);
-  p.items = static_cast<const zl::Item*>(plan->dev);
-  p.n_items = plan->n_items;
+  p.dsum = static_cast<float*>(workspace);
+  const char* base = static_cast<const char*>(plan->dev);
+  p.kv_items = reinterpret_cast<const zl::Item*>(base);
+  p.n_kv_items = plan->n_items;
+  p.q_items = reinterpret_cast<const zl::Item*>(base + plan->slots_offset);
+  p.n_q_items = plan->n_items2;
+  p.cu_k = reinterpret_cast<const int32_t*>(base + plan->cuk_offset);
+  p.seg_ranges = reinterpret_cast<const zl::SegRanges*>(base + plan->ranges_offset);
   p.num_heads = H;
   p.total_q = sh.total_q;
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
   p.xcd_chunk = 1;
   hipError_t e = timed(ZL_K_BWD_PRE, s, [&] { return zl::launch_bwd_bf16(p, hd, 0, s); });
-  if (e == hipSuccess) e = timed(ZL_K_BWD_MAIN, s, [&] { return zl::launch_bwd_bf16(p, hd, 1, s); });
-  if (e == hipSuccess) e = timed(ZL_K_BWD_FIN, s, [&] { return zl::launch_bwd_bf16(p, hd, 2, s); });
+  if (e == hipSuccess) e = timed(ZL_K_BWD_DKDV, s, [&] { return zl::launch_bwd_bf16(p, hd, 1, s); });
+  if (e == hipSuccess) e = timed(ZL_K_BWD_DQ, s, [&] { return zl::launch_bwd_bf16(p, hd, 2, s); });
   return hip_status(e, "backward launch");
 }
 
@@ -496,7 +528,8 @@ zl_status zl_plan_dump(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype 
                        size_t cap, size_t* n, int32_t* tile_m, int32_t* tile_n) {
   zl_status st = validate_common(H, hd, dt, 1.f, false);
   if (st != ZL_OK) return st;
-  if (op != ZL_OP_FWD && op != ZL_OP_BWD) return fail(ZL_ERR_INVALID_ARG, "op must be ZL_OP_FWD or ZL_OP_BWD");
+  if (op != ZL_OP_FWD && op != ZL_OP_BWD && op != ZL_OP_BWD_DQ)
+    return fail(ZL_ERR_INVALID_ARG, "op must be ZL_OP_FWD, ZL_OP_BWD or ZL_OP_BWD_DQ");
   if (!n) return fail(ZL_ERR_INVALID_ARG, "n is NULL");
   if (cap > 0 && !items) return fail(ZL_ERR_INVALID_ARG, "items is NULL with cap > 0");
   Shape sh;

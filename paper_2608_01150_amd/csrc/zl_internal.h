@@ -24,8 +24,10 @@ constexpr int kFwdTileM = 128;       // bf16 forward: 4 waves x 32 query rows
 constexpr int kFwdTileN = 64;        // keys per inner step
 constexpr int kFwd32TileM = 64;      // fp32 forward: one query row per lane
 constexpr int kFwd32TileN = 32;
-constexpr int kBwdTileN = 128;       // bf16 backward: 4 waves x 32 keys
-constexpr int kBwdTileM = 32;        // queries per inner step
+constexpr int kBwdTileN = 128;       // dK/dV kernel: 4 waves x 32 keys per item
+constexpr int kBwdTileM = 64;        // queries per dK/dV inner step
+constexpr int kDqTileM = 128;        // dQ kernel: 4 waves x 32 query rows per item
+constexpr int kDqTileN = 64;         // keys per dQ inner step
 
 // Work-item index of workgroup `b`.  Workgroups are dispatched round-robin
 // over the 8 XCDs (b % 8); each run of 8*chunk consecutive workgroups is
@@ -78,6 +80,11 @@ struct MergeParams {
   int64_t lse_slot_stride;
 };
 
+// The K/V ranges a query segment attends to: kv_first .. kv_first+kv_count-1.
+struct SegRanges {
+  int32_t kv_first, kv_count;
+};
+
 struct BwdParams {
   const void* q;
   const void* k;
@@ -88,12 +95,15 @@ struct BwdParams {
   void* dq;
   void* dk;
   void* dv;
-  float* dq_acc;     // [Tq, H, d] fp32 workspace
-  float* dsum;       // [Tq, H] fp32 workspace: D = rowsum(dO * O)
-  const Item* items;
-  int32_t n_items;
+  float* dsum;                 // [Tq, H] fp32 workspace: D = rowsum(dO * O)
+  const Item* kv_items;        // dK/dV items: one key tile against all of its segment's queries
+  int32_t n_kv_items;
+  const Item* q_items;         // dQ items: one query tile against every key of its segment
+  int32_t n_q_items;
+  const int32_t* cu_k;         // device copy of cu_seqlens_k
+  const SegRanges* seg_ranges; // per query segment
   int32_t num_heads;
-  int64_t total_q;   // Tq
+  int64_t total_q;             // Tq
   float scale;
   float scale_log2;
   int32_t xcd_chunk;
@@ -102,7 +112,7 @@ struct BwdParams {
 hipError_t launch_fwd_bf16(const FwdParams& p, int head_dim, hipStream_t s);
 hipError_t launch_fwd_fp32(const FwdParams& p, int head_dim, hipStream_t s);
 hipError_t launch_merge(const MergeParams& p, int head_dim, bool out_bf16, hipStream_t s);
-// stage 0: preprocess, 1: main, 2: dQ finalize
+// stage 0: preprocess (D), 1: dK/dV, 2: dQ
 hipError_t launch_bwd_bf16(const BwdParams& p, int head_dim, int stage, hipStream_t s);
 
 }  // namespace zl

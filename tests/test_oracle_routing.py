@@ -41,6 +41,19 @@ def test_items_cover_every_pair_once(op, bm, bn):
     assert costs == sorted(costs, reverse=True)
 
 
+def test_dq_items_cover_each_row_once_with_all_keys():
+    items = oracle.work_items(DESC, 2, 2, 128, 64)
+    rows = collections.Counter()
+    for (q0, ql, k0, kl, h, slot, s, j) in items:
+        assert slot == -1 and j == DESC["kv_first"][s]
+        first, count = DESC["kv_first"][s], DESC["kv_count"][s]
+        ck = DESC["cu_seqlens_k"]
+        assert kl == ck[first + count] - ck[first] and k0 == ck[first]
+        for r in range(q0, q0 + ql):
+            rows[(r, h)] += 1
+    assert rows == collections.Counter({(r, h): 1 for r in range(428) for h in range(2)})
+
+
 def test_slots_follow_block_index():
     for (q0, ql, k0, kl, h, slot, s, j) in oracle.work_items(DESC, 1, 0, 128, 64):
         assert slot == (DESC["block_index"][j] if DESC["kind"][s] == 1 else -1)

@@ -21,7 +21,7 @@ def _compare(d, H, hd, dtype, op):
 @pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
 def test_workload_schedules_match_oracle(name):
     w = W.get(name)
-    ops = [api.ZL_OP_FWD] + ([api.ZL_OP_BWD] if w.backward else [])
+    ops = [api.ZL_OP_FWD] + ([api.ZL_OP_BWD, api.ZL_OP_BWD_DQ] if w.backward else [])
     for op in ops:
         items, tm, tn = _compare(w.desc_dict() | {"q_offset": w.q_offset, "k_offset": w.k_offset},
                                  w.num_heads, w.head_dim, w.torch_dtype, op)
@@ -35,9 +35,9 @@ def test_random_descriptor_schedules_match_oracle():
         d = _descs.random_desc(rng, int(rng.integers(0, 5)), int(rng.integers(0, 4)), 300, 5)
         if not d["kind"]:
             continue
-        for op in (api.ZL_OP_FWD, api.ZL_OP_BWD):
+        for op in (api.ZL_OP_FWD, api.ZL_OP_BWD, api.ZL_OP_BWD_DQ):
             for dtype in (torch.bfloat16, torch.float32):
-                if op == api.ZL_OP_BWD and dtype == torch.float32:
+                if op != api.ZL_OP_FWD and dtype == torch.float32:
                     continue
                 _compare(d, int(rng.integers(1, 4)), 64, dtype, op)
 
