@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--workload", default="c4", help="c2..c5 (default c4: coalesced whole+shard)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-heads", type=int, default=1)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (for scaling HBM byte counters)")
     return ap.parse_args()
 
 
@@ -102,6 +104,14 @@ def main():
               "--gpus must be 1.", file=sys.stderr)
         sys.exit(2)
     import torch
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n}), flush=True)
+        return
     from paper_2608_01150_amd import api
     from paper_2608_01150_amd import workloads as W
 

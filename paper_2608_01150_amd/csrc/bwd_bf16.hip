@@ -17,10 +17,10 @@
 //                    dS^T = P^T (dP^T - D)
 //                    dQ^T += K^T dS^T                 MFMA
 //                  A shard row sums its blocks inside one item.
-// Q/dO (dK/dV) and K/V (dQ) tiles are staged row-major in double-buffered LDS,
-// the next tile fetched into registers while the current one computes; the
-// transposed operands (Q^T, dO^T, K^T) come straight from the row-major
-// tiles through LDS transpose reads.
+// Q/dO (dK/dV) and K/V (dQ) tiles are staged row-major (padded pitch,
+// conflict-free) in double-buffered LDS, the next tile fetched into registers
+// while the current one computes; the transposed operands (Q^T, dO^T, K^T)
+// come straight from the row-major tiles through LDS transpose reads.
 
 #include <algorithm>
 
@@ -52,24 +52,15 @@ __global__ __launch_bounds__(NT) void bwd_pre_kernel(BwdParams p) {
   if (live && sub == 0) p.dsum[u] = acc;
 }
 
-// Byte offset of element (row, col) of a row-major [rows][D] bf16 tile whose
-// 16-byte chunks are XOR-swizzled by swz(row).
-template <int D>
-__device__ __forceinline__ uint32_t rm_off(int row, int col) {
-  return row * (D * 2) + ((((col >> 3) ^ swz(row))) << 4) + (col & 7) * 2;
-}
-
-template <int D>
-struct RowMajor {
-  __device__ __forceinline__ uint32_t operator()(int row, int col) const { return rm_off<D>(row, col); }
-};
-
 // ------------------------------------------------------------------ dK / dV
 template <int D>
 __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   constexpr int BQ = kBwdTileM;                 // 64 queries per step
-  constexpr int TILE = BQ * D * 2;              // bytes of one Q (or dO) tile
-  constexpr int CH = BQ * D / 8 / NT;           // 16-byte chunks per thread per tile
+  constexpr int PITCH = Pad<D>::PITCH;
+  constexpr int TILE = BQ * PITCH;              // bytes of one Q (or dO) tile
+  constexpr int CPR = D / 8;                    // 16-byte chunks per row
+  constexpr int CH = BQ * CPR / NT;             // chunks per thread per tile
+  constexpr int RSTEP = NT / CPR;
   __shared__ __attribute__((aligned(16))) char qs[2][TILE];
   __shared__ __attribute__((aligned(16))) char dos[2][TILE];
   __shared__ __attribute__((aligned(16))) float lse2s[2][BQ];
@@ -103,16 +94,23 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
     dv[db] = f32x16{};
   }
 
+  const int srow = tid / CPR, scol = tid % CPR;
+  const uint32_t st_off = poff<D>(srow, scol * 8);
+  const uint32_t a_off = poff<D>(perm32(ln), g * 8);
+  const uint32_t t_off = tr_lane_off<D>(lane);
+  const int64_t g_off = srow * rs + scol * 8;
+
   u32x4 qreg[CH], oreg[CH];
   float sreg = 0.f;
   auto fetch = [&](int q0) {
     const int nq = it.q_len - q0;
+    const uint16_t* qb_ = qg + q0 * rs + g_off;
+    const uint16_t* ob_ = dog + q0 * rs + g_off;
 #pragma unroll
     for (int r = 0; r < CH; ++r) {
-      const int c = tid + r * NT, row = c / (D / 8), col = c % (D / 8);
-      const bool ok = row < nq;
-      qreg[r] = ok ? *reinterpret_cast<const u32x4*>(qg + (q0 + row) * rs + col * 8) : u32x4{0, 0, 0, 0};
-      oreg[r] = ok ? *reinterpret_cast<const u32x4*>(dog + (q0 + row) * rs + col * 8) : u32x4{0, 0, 0, 0};
+      const bool ok = srow + r * RSTEP < nq;
+      qreg[r] = ok ? *reinterpret_cast<const u32x4*>(qb_ + r * RSTEP * rs) : u32x4{0, 0, 0, 0};
+      oreg[r] = ok ? *reinterpret_cast<const u32x4*>(ob_ + r * RSTEP * rs) : u32x4{0, 0, 0, 0};
     }
     if (tid < BQ) {
       // rows past the segment: LSE = +big makes P = 0 there
@@ -124,9 +122,8 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   auto stash = [&](int buf) {
 #pragma unroll
     for (int r = 0; r < CH; ++r) {
-      const int c = tid + r * NT, row = c / (D / 8), col = c % (D / 8);
-      *reinterpret_cast<u32x4*>(qs[buf] + rm_off<D>(row, col * 8)) = qreg[r];
-      *reinterpret_cast<u32x4*>(dos[buf] + rm_off<D>(row, col * 8)) = oreg[r];
+      *reinterpret_cast<u32x4*>(qs[buf] + st_off + r * RSTEP * PITCH) = qreg[r];
+      *reinterpret_cast<u32x4*>(dos[buf] + st_off + r * RSTEP * PITCH) = oreg[r];
     }
     if (tid < BQ) lse2s[buf][tid] = sreg;
     else if (tid < 2 * BQ) dsums[buf][tid - BQ] = sreg;
@@ -139,19 +136,18 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
     __syncthreads();  // tile `buf` is complete; tile buf^1 is no longer read
     const bool more = q0 + BQ < it.q_len;
     if (more) fetch(q0 + BQ);
-    const char* qt = qs[buf];
-    const char* ot = dos[buf];
+    const char* qa = qs[buf] + a_off;
+    const char* oa = dos[buf] + a_off;
+    const char* qt = qs[buf] + t_off;
+    const char* ot = dos[buf] + t_off;
 #pragma unroll
     for (int sb = 0; sb < BQ / 32; ++sb) {
       // S and dP: D row m <-> query sb*32 + perm32(m); register i <-> query sb*32 + 16*(i/8) + 8g + i%8.
       f32x16 s = f32x16{}, dp = f32x16{};
-      const int qrow = sb * 32 + perm32(ln);
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(qt + rm_off<D>(qrow, kk * 16 + g * 8));
-        s = mfma32(a, kf[kk], s);
-        const u32x4 b = *reinterpret_cast<const u32x4*>(ot + rm_off<D>(qrow, kk * 16 + g * 8));
-        dp = mfma32(b, vf[kk], dp);
+        s = mfma32(*reinterpret_cast<const u32x4*>(qa + poff<D>(sb * 32, kk * 16)), kf[kk], s);
+        dp = mfma32(*reinterpret_cast<const u32x4*>(oa + poff<D>(sb * 32, kk * 16)), vf[kk], dp);
       }
       u32x4 pp[2], pds[2];
 #pragma unroll
@@ -169,7 +165,7 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
             const int tt = 2 * t + e, i = 8 * h + tt;
             const float l2 = tt < 4 ? l0[tt] : l1[tt - 4];
             const float dd = tt < 4 ? d0[tt] : d1[tt - 4];
-            const float pr = k_ok ? fast_exp2(s[i] * p.scale_log2 - l2) : 0.f;
+            const float pr = k_ok ? fast_exp2(fmaf(s[i], p.scale_log2, -l2)) : 0.f;
             pv[e] = pr;
             dsv[e] = pr * (dp[i] - dd);
           }
@@ -182,9 +178,8 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
       for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const int k0 = sb * 32 + 16 * h;
-          dv[db] = mfma32(tr_operand(ot, k0, db * 32, lane, RowMajor<D>{}), pp[h], dv[db]);
-          dk[db] = mfma32(tr_operand(qt, k0, db * 32, lane, RowMajor<D>{}), pds[h], dk[db]);
+          dv[db] = mfma32(tr_operand<D>(ot, sb * 32 + 16 * h, db * 32), pp[h], dv[db]);
+          dk[db] = mfma32(tr_operand<D>(qt, sb * 32 + 16 * h, db * 32), pds[h], dk[db]);
         }
       }
     }
@@ -215,8 +210,11 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
 template <int D>
 __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
   constexpr int BN = kDqTileN;                  // 64 keys per step
-  constexpr int TILE = BN * D * 2;
-  constexpr int CH = BN * D / 8 / NT;
+  constexpr int PITCH = Pad<D>::PITCH;
+  constexpr int TILE = BN * PITCH;
+  constexpr int CPR = D / 8;
+  constexpr int CH = BN * CPR / NT;
+  constexpr int RSTEP = NT / CPR;
   __shared__ __attribute__((aligned(16))) char ks[2][TILE];
   __shared__ __attribute__((aligned(16))) char vs[2][TILE];
 
@@ -245,6 +243,12 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) dq[db] = f32x16{};
 
+  const int srow = tid / CPR, scol = tid % CPR;
+  const uint32_t st_off = poff<D>(srow, scol * 8);
+  const uint32_t a_off = poff<D>(perm32(ln), g * 8);
+  const uint32_t t_off = tr_lane_off<D>(lane);
+  const int64_t g_off = srow * rs + scol * 8;
+
   // Key tiles run over the segment's ranges in order; (r, kt) is the tile
   // [cu_k[r] + kt, cu_k[r] + kt + BN) clipped to the range.
   const int r_end = sr.kv_first + sr.kv_count;
@@ -259,22 +263,20 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
   u32x4 kreg[CH], vreg[CH];
   auto fetch = [&](int r, int kt) {
     const int k0 = p.cu_k[r] + kt, nvalid = p.cu_k[r + 1] - k0;
-    const uint16_t* kgp = static_cast<const uint16_t*>(p.k) + ((int64_t)k0 * H + it.head) * D;
-    const uint16_t* vgp = static_cast<const uint16_t*>(p.v) + ((int64_t)k0 * H + it.head) * D;
+    const uint16_t* kb_ = static_cast<const uint16_t*>(p.k) + ((int64_t)k0 * H + it.head) * D + g_off;
+    const uint16_t* vb_ = static_cast<const uint16_t*>(p.v) + ((int64_t)k0 * H + it.head) * D + g_off;
 #pragma unroll
     for (int c8 = 0; c8 < CH; ++c8) {
-      const int c = tid + c8 * NT, row = c / (D / 8), col = c % (D / 8);
-      const bool ok = row < nvalid;
-      kreg[c8] = ok ? *reinterpret_cast<const u32x4*>(kgp + row * rs + col * 8) : u32x4{0, 0, 0, 0};
-      vreg[c8] = ok ? *reinterpret_cast<const u32x4*>(vgp + row * rs + col * 8) : u32x4{0, 0, 0, 0};
+      const bool ok = srow + c8 * RSTEP < nvalid;
+      kreg[c8] = ok ? *reinterpret_cast<const u32x4*>(kb_ + c8 * RSTEP * rs) : u32x4{0, 0, 0, 0};
+      vreg[c8] = ok ? *reinterpret_cast<const u32x4*>(vb_ + c8 * RSTEP * rs) : u32x4{0, 0, 0, 0};
     }
   };
   auto stash = [&](int buf) {
 #pragma unroll
     for (int c8 = 0; c8 < CH; ++c8) {
-      const int c = tid + c8 * NT, row = c / (D / 8), col = c % (D / 8);
-      *reinterpret_cast<u32x4*>(ks[buf] + rm_off<D>(row, col * 8)) = kreg[c8];
-      *reinterpret_cast<u32x4*>(vs[buf] + rm_off<D>(row, col * 8)) = vreg[c8];
+      *reinterpret_cast<u32x4*>(ks[buf] + st_off + c8 * RSTEP * PITCH) = kreg[c8];
+      *reinterpret_cast<u32x4*>(vs[buf] + st_off + c8 * RSTEP * PITCH) = vreg[c8];
     }
   };
 
@@ -292,21 +294,19 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
     first_tile(r, kt + BN, &rn, &ktn);
     const bool more = rn < r_end;
     if (more) fetch(rn, ktn);
-    const char* kt_ = ks[buf];
-    const char* vt_ = vs[buf];
+    const char* ka = ks[buf] + a_off;
+    const char* va = vs[buf] + a_off;
+    const char* kt_ = ks[buf] + t_off;
 
     // S^T and dP^T for keys [kb*32, kb*32+32): D row m <-> key kb*32 + perm32(m).
     u32x4 pds[2][2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       f32x16 s = f32x16{}, dp = f32x16{};
-      const int krow = kb * 32 + perm32(ln);
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(kt_ + rm_off<D>(krow, kk * 16 + g * 8));
-        s = mfma32(a, qf[kk], s);
-        const u32x4 b = *reinterpret_cast<const u32x4*>(vt_ + rm_off<D>(krow, kk * 16 + g * 8));
-        dp = mfma32(b, of[kk], dp);
+        s = mfma32(*reinterpret_cast<const u32x4*>(ka + poff<D>(kb * 32, kk * 16)), qf[kk], s);
+        dp = mfma32(*reinterpret_cast<const u32x4*>(va + poff<D>(kb * 32, kk * 16)), of[kk], dp);
       }
       // register i <-> key kb*32 + 16*(i/8) + 8g + i%8 of this tile, query = lane's row
 #pragma unroll
@@ -315,8 +315,8 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
           const int keyi = kb * 32 + 16 * ((i + u) >> 3) + 8 * g + ((i + u) & 7);
-          const float pr = keyi < nvalid ? fast_exp2(s[i + u] * p.scale_log2 - lse2) : 0.f;
-          e[u] = pr * (dp[i + u] - dd);
+          const float pr = fast_exp2(fmaf(s[i + u], p.scale_log2, -lse2));
+          e[u] = (nvalid >= BN || keyi < nvalid) ? pr * (dp[i + u] - dd) : 0.f;
         }
         pds[kb][i >> 3][(i & 7) >> 1] = pack_bf16(e[0], e[1]);
       }
@@ -327,9 +327,8 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          dq[db] = mfma32(tr_operand(kt_, kb * 32 + 16 * s2, db * 32, lane, RowMajor<D>{}), pds[kb][s2], dq[db]);
-        }
+        for (int s2 = 0; s2 < 2; ++s2)
+          dq[db] = mfma32(tr_operand<D>(kt_, kb * 32 + 16 * s2, db * 32), pds[kb][s2], dq[db]);
       }
     }
     if (more) stash(buf ^ 1);

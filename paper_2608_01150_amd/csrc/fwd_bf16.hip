@@ -6,11 +6,14 @@
 // rows.  Per 64-key step:
 //   S^T = K Q^T          MFMA 32x32x16 bf16, K from LDS (A), Q in registers (B)
 //   online softmax       per query in the lane's registers (exp2 domain)
-//   O^T += V^T P^T       MFMA, V^T from LDS (A), P^T straight from registers (B)
+//   O^T += V^T P^T       MFMA, V^T from LDS by transpose reads (A), P^T
+//                        straight from registers (B)
 // Computing the transposed products keeps one query per lane, so the row max
 // needs a single cross-lane exchange (lanes l and l^32) and the softmax
-// output is already the B operand of the next MFMA.  K and V tiles for the
-// next step are fetched into registers while the current step computes.
+// output is already the B operand of the next MFMA.  K and V tiles are staged
+// row-major (padded pitch, conflict-free) in double-buffered LDS; the next
+// tile is fetched into registers while the current one computes, one barrier
+// per step.
 //
 // Epilogue: WHOLE items write the final bf16 output and the LSE; SHARD items
 // write the block-normalised fp32 partial and its LSE into their CP slot.
@@ -21,30 +24,23 @@
 namespace zl {
 namespace {
 
-constexpr int BM = kFwdTileM;
 constexpr int BN = kFwdTileN;
 constexpr int NT = 256;
 
-template <int D>
-struct FwdTile {
-  static constexpr int KCH = D / 8;                  // 16-byte chunks per K row
-  static constexpr int K_LOADS = BN * KCH / NT;      // 16-byte K chunks per thread
-  static constexpr int V_UNITS = (BN / 2) * KCH / NT;  // (key pair, chunk) units per thread
-};
-
-// Byte offset of 16-byte chunk `c` of K row `r` in the swizzled K tile.
-template <int D>
-__device__ __forceinline__ uint32_t k_off(int r, int c) {
-  return r * (D * 2) + ((c ^ swz(r)) << 4);
-}
-// Byte offset of 16-byte chunk `c` (8 keys) of V^T row `d` (64 keys = 128 B).
-__device__ __forceinline__ uint32_t vt_off(int d, int c) { return d * (BN * 2) + ((c ^ swz(d)) << 4); }
+// Rescale the running output only when the running maximum grows by more
+// than 2^8 (log2 units): exp2 of scores against a stale maximum stays below
+// 2^8, exact in fp32 and bf16 range, and O and l share the same reference.
+constexpr float kRescaleSlack = 8.f;
 
 template <int D>
 __global__ __launch_bounds__(NT, 2) void fwd_bf16_kernel(FwdParams p) {
-  using T = FwdTile<D>;
-  __shared__ __attribute__((aligned(16))) char smem_k[BN * D * 2];
-  __shared__ __attribute__((aligned(16))) char smem_vt[D * BN * 2];
+  constexpr int PITCH = Pad<D>::PITCH;
+  constexpr int TILE = BN * PITCH;
+  constexpr int CPR = D / 8;           // 16-byte chunks per row
+  constexpr int CH = BN * CPR / NT;    // chunks per thread per tile
+  constexpr int RSTEP = NT / CPR;      // rows between a thread's chunks
+  __shared__ __attribute__((aligned(16))) char ks[2][TILE];
+  __shared__ __attribute__((aligned(16))) char vs[2][TILE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ln = lane & 31, g = lane >> 5;
@@ -59,122 +55,116 @@ __global__ __launch_bounds__(NT, 2) void fwd_bf16_kernel(FwdParams p) {
   const bool q_ok = qr < it.q_len;
   u32x4 qf[D / 16];
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
+  for (int kk = 0; kk < D / 16; ++kk)
     qf[kk] = q_ok ? *reinterpret_cast<const u32x4*>(qg + qr * rs + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
-  }
 
   float m_run = kNegBig, l_part = 0.f;
   f32x16 o[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) o[db] = f32x16{};
 
-  u32x4 kreg[T::K_LOADS];
-  u32x4 vreg[T::V_UNITS][2];
+  // Per-lane LDS offsets: staging chunk, A-operand row perm32(ln), transpose piece.
+  const int srow = tid / CPR, scol = tid % CPR;
+  const uint32_t st_off = poff<D>(srow, scol * 8);
+  const uint32_t a_off = poff<D>(perm32(ln), g * 8);
+  const uint32_t t_off = tr_lane_off<D>(lane);
+  const int64_t g_off = srow * rs + scol * 8;
 
+  u32x4 kreg[CH], vreg[CH];
   auto fetch = [&](int kt) {
     const int nvalid = it.k_len - kt;
+    const uint16_t* kb_ = kg + kt * rs + g_off;
+    const uint16_t* vb_ = vg + kt * rs + g_off;
 #pragma unroll
-    for (int r = 0; r < T::K_LOADS; ++r) {
-      const int c = tid + r * NT, row = c / T::KCH, col = c % T::KCH;
-      kreg[r] = row < nvalid ? *reinterpret_cast<const u32x4*>(kg + (kt + row) * rs + col * 8) : u32x4{0, 0, 0, 0};
+    for (int r = 0; r < CH; ++r) {
+      const bool ok = srow + r * RSTEP < nvalid;
+      kreg[r] = ok ? *reinterpret_cast<const u32x4*>(kb_ + r * RSTEP * rs) : u32x4{0, 0, 0, 0};
+      vreg[r] = ok ? *reinterpret_cast<const u32x4*>(vb_ + r * RSTEP * rs) : u32x4{0, 0, 0, 0};
     }
+  };
+  auto stash = [&](int buf) {
 #pragma unroll
-    for (int r = 0; r < T::V_UNITS; ++r) {
-      const int u = tid + r * NT, pr = u % (BN / 2), cc = u / (BN / 2);
-      const int k0 = 2 * pr;
-      vreg[r][0] = k0 < nvalid ? *reinterpret_cast<const u32x4*>(vg + (kt + k0) * rs + cc * 8) : u32x4{0, 0, 0, 0};
-      vreg[r][1] = k0 + 1 < nvalid ? *reinterpret_cast<const u32x4*>(vg + (kt + k0 + 1) * rs + cc * 8)
-                                   : u32x4{0, 0, 0, 0};
+    for (int r = 0; r < CH; ++r) {
+      *reinterpret_cast<u32x4*>(ks[buf] + st_off + r * RSTEP * PITCH) = kreg[r];
+      *reinterpret_cast<u32x4*>(vs[buf] + st_off + r * RSTEP * PITCH) = vreg[r];
     }
   };
 
-  auto stash = [&]() {
-#pragma unroll
-    for (int r = 0; r < T::K_LOADS; ++r) {
-      const int c = tid + r * NT, row = c / T::KCH, col = c % T::KCH;
-      *reinterpret_cast<u32x4*>(smem_k + k_off<D>(row, col)) = kreg[r];
-    }
-#pragma unroll
-    for (int r = 0; r < T::V_UNITS; ++r) {
-      const int u = tid + r * NT, pr = u % (BN / 2), cc = u / (BN / 2);
-      // keys 2pr, 2pr+1 of d = 8cc+j go to V^T row 8cc+j as one dword
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t a = vreg[r][0][j >> 1], b = vreg[r][1][j >> 1];
-        const uint32_t w = (j & 1) ? ((a >> 16) | (b & 0xFFFF0000u)) : ((a & 0xFFFFu) | (b << 16));
-        const int d = cc * 8 + j;
-        *reinterpret_cast<uint32_t*>(smem_vt + vt_off(d, pr >> 2) + (pr & 3) * 4) = w;
-      }
-    }
-  };
-
-  if (it.k_len > 0) fetch(0);
-  for (int kt = 0; kt < it.k_len; kt += BN) {
-    __syncthreads();
-    stash();
-    __syncthreads();
-    if (kt + BN < it.k_len) fetch(kt + BN);
+  if (it.k_len > 0) {
+    fetch(0);
+    stash(0);
+  }
+  int buf = 0;
+  for (int kt = 0; kt < it.k_len; kt += BN, buf ^= 1) {
+    __syncthreads();  // tile `buf` is complete; tile buf^1 is no longer read
+    const bool more = kt + BN < it.k_len;
+    if (more) fetch(kt + BN);
+    const char* ka = ks[buf] + a_off;
+    const char* vt = vs[buf] + t_off;
 
     // S^T for keys [kb*32, kb*32+32): D row m <-> key kb*32 + perm32(m).
     f32x16 s[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       s[kb] = f32x16{};
-      const int krow = kb * 32 + perm32(ln);
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(smem_k + k_off<D>(krow, 2 * kk + g));
-        s[kb] = mfma32(a, qf[kk], s[kb]);
+      for (int kk = 0; kk < D / 16; ++kk)
+        s[kb] = mfma32(*reinterpret_cast<const u32x4*>(ka + poff<D>(kb * 32, kk * 16)), qf[kk], s[kb]);
+    }
+    // s[kb][i] is the raw score of (key kb*32 + 16*(i/8) + 8*g + i%8, query qr).
+    const int nvalid = it.k_len - kt;
+    if (nvalid < BN) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = kb * 32 + 16 * (i >> 3) + 8 * g + (i & 7);
+          if (key >= nvalid) s[kb][i] = kNegBig;
+        }
       }
     }
-    // s[kb][i] is (key kb*32 + 16*(i/8) + 8*g + i%8, query qr).
-    const int nvalid = it.k_len - kt;
     float mt = kNegBig;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = kb * 32 + 16 * (i >> 3) + 8 * g + (i & 7);
-        float x = s[kb][i] * p.scale_log2;
-        if (nvalid < BN && key >= nvalid) x = kNegBig;
-        s[kb][i] = x;
-        mt = fmaxf(mt, x);
+      for (int i = 0; i < 16; ++i) mt = fmaxf(mt, s[kb][i]);
+    }
+    mt = fmaxf(mt, __shfl_xor(mt, 32)) * p.scale_log2;
+    if (__any(mt > m_run + kRescaleSlack)) {
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = fast_exp2(m_run - m_new);
+      m_run = m_new;
+      l_part *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
       }
     }
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = fast_exp2(m_run - m_new);
-    m_run = m_new;
     float lsum = 0.f;
     u32x4 pb[2][2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int i = 0; i < 16; i += 2) {
-        const float e0 = fast_exp2(s[kb][i] - m_new), e1 = fast_exp2(s[kb][i + 1] - m_new);
+        const float e0 = fast_exp2(fmaf(s[kb][i], p.scale_log2, -m_run));
+        const float e1 = fast_exp2(fmaf(s[kb][i + 1], p.scale_log2, -m_run));
         lsum += e0 + e1;
         pb[kb][i >> 3][(i & 7) >> 1] = pack_bf16(e0, e1);
       }
     }
-    l_part = l_part * alpha + lsum;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
-    }
+    l_part += lsum;
     // O^T[d, q] += sum_key V^T[d, key] P^T[key, q]; A row m <-> d = db*32 + perm32(m).
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
-      const int vrow = db * 32 + perm32(ln);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          const u32x4 a = *reinterpret_cast<const u32x4*>(smem_vt + vt_off(vrow, 4 * kb + 2 * s2 + g));
-          o[db] = mfma32(a, pb[kb][s2], o[db]);
-        }
+        for (int s2 = 0; s2 < 2; ++s2)
+          o[db] = mfma32(tr_operand<D>(vt, kb * 32 + 16 * s2, db * 32), pb[kb][s2], o[db]);
       }
     }
+    if (more) stash(buf ^ 1);
   }
 
   // Epilogue.  o[db][i] is (d = db*32 + 16*(i/8) + 8*g + i%8, query qr).

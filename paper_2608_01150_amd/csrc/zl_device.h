@@ -41,9 +41,22 @@ __device__ __forceinline__ int perm32(int m) {
   return ((blk4 >> 1) << 4) + (g << 3) + ((blk4 & 1) << 2) + lo;
 }
 
-// XOR swizzle of 16-byte chunks within an LDS row, keyed by the row index:
-// the 8 rows perm32 sends to 8 consecutive lanes land on 8 distinct chunks.
-__device__ __forceinline__ int swz(int row) { return (row ^ ((row >> 3) << 2)) & 7; }
+// Row-major bf16 LDS tile with a padded row pitch: 304 bytes for D = 128
+// (256 + 48), 144 for D = 64.  With 64 four-byte banks and 16 lanes served
+// per cycle, both MFMA operand access patterns are conflict-free:
+//  * A-operand 16-byte reads, where 16 lanes read one 16-byte chunk from the
+//    16 rows perm32 gives them, and
+//  * transpose reads, where 16 lanes read 4 consecutive rows x 32 bytes.
+// Every address is a per-lane base plus a compile-time offset, so the loops
+// do no address arithmetic.
+template <int D>
+struct Pad {
+  static constexpr int PITCH = D == 128 ? 304 : 144;
+};
+template <int D>
+__device__ __forceinline__ constexpr uint32_t poff(int row, int col) {
+  return row * Pad<D>::PITCH + col * 2;
+}
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
@@ -55,19 +68,26 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const void* p) {
   return __builtin_bit_cast(u32x2, v);
 }
 
-// MFMA operand whose 8 k-values run down a column of a row-major [k][col]
-// bf16 LDS tile: lane l (m = l%32, g = l/32) receives rows k0 + 8g .. k0 + 8g
-// + 7 of column col_base + perm32(m).  `off(row, col)` is the tile's byte
-// offset of element (row, col); 4 consecutive columns must be 8-byte
-// contiguous.  Two transpose reads, each lane addressing one 8-byte piece of
-// a 4-row x 16-column block.
-template <class Off>
-__device__ __forceinline__ u32x4 tr_operand(const char* tile, int k0, int col_base, int lane, Off off) {
+// Per-lane byte offset for tr_operand on a padded [k][D] tile.  A lane's
+// transpose-read piece is row 8*g + i/4 and 4 columns starting at
+// perm32(16*(i/16 % 2) + 4*(i%4)), with i the lane's index within its
+// 16-lane group.
+template <int D>
+__device__ __forceinline__ uint32_t tr_lane_off(int lane) {
   const int grp = lane >> 4, i = lane & 15;
-  const int row = k0 + 8 * (lane >> 5) + (i >> 2);
-  const int col = col_base + perm32(16 * (grp & 1) + 4 * (i & 3));
-  const u32x2 lo = lds_read_tr16(tile + off(row, col));
-  const u32x2 hi = lds_read_tr16(tile + off(row + 4, col));
+  return poff<D>(8 * (lane >> 5) + (i >> 2), perm32(16 * (grp & 1) + 4 * (i & 3)));
+}
+
+// MFMA operand whose 8 k-values run down a column of a row-major [k][D] LDS
+// tile: lane l (m = l%32, g = l/32) receives rows k0 + 8g .. k0 + 8g + 7 of
+// column col_base + perm32(m).  `lane_ptr` is the tile base plus
+// tr_lane_off(lane); k0 and col_base are compile-time after unrolling.  Two
+// transpose reads, each lane addressing one 8-byte piece of a 4-row x
+// 16-column block.
+template <int D>
+__device__ __forceinline__ u32x4 tr_operand(const char* lane_ptr, int k0, int col_base) {
+  const u32x2 lo = lds_read_tr16(lane_ptr + poff<D>(k0, col_base));
+  const u32x2 hi = lds_read_tr16(lane_ptr + poff<D>(k0 + 4, col_base));
   return u32x4{lo[0], lo[1], hi[0], hi[1]};
 }
 
