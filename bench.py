@@ -15,7 +15,7 @@ HIP events on its own stream inside the timed region and priced at the MFMA
 FLOPs it executes per pair (forward 4d, dK/dV 8d, dQ 6d) against the bf16
 dense MFMA peak.
 cpu_baseline = the fp64 oracle timed on this host's cores on a bounded
-sample of the same batch (see --cpu-sample-heads).
+sample of the same batch (see --cpu-seconds).
 """
 from __future__ import annotations
 
@@ -37,19 +37,22 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c4", help="c2..c5 (default c4: coalesced whole+shard)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-heads", type=int, default=1)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="accumulate oracle heads until this much CPU time is spent")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (for scaling HBM byte counters)")
     return ap.parse_args()
 
 
-def cpu_baseline(w, heads):
+def cpu_baseline(w, min_seconds):
     """Time the oracle (as it stands) on a bounded sample of workload w.
 
-    Sample: `heads` head(s); every whole segment in full (forward+backward);
-    each shard reduced to its first 1/9 of query rows, forward against all of
-    its blocks, merge, and backward against all blocks.  FLOPs are counted
-    with the same convention as the GPU value (14*d per pair).
+    Sample: heads taken one at a time until at least `min_seconds` of oracle
+    time has accumulated (or every head is done); per head, every whole
+    segment in full (forward + backward) and each shard reduced to its first
+    1/9 of query rows, forward against all of its blocks, merge, backward
+    against all blocks.  FLOPs are counted with the same convention as the
+    GPU value (14*d per pair).
     """
     import numpy as np
     import oracle
@@ -60,10 +63,8 @@ def cpu_baseline(w, heads):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count() or 1])
     except Exception:  # pragma: no cover
         cores = os.cpu_count() or 1
-    hs = list(range(heads))
     d = w.desc_dict()
     cq = list(d["cu_seqlens_q"])
-    # shrink shard query rows: keep the first ceil(L/9) rows of each shard
     new_cq, rows = [0], []
     for s in range(w.num_segments):
         a, b = cq[s], cq[s + 1]
@@ -72,28 +73,31 @@ def cpu_baseline(w, heads):
         rows.append((a, b))
         new_cq.append(new_cq[-1] + (b - a))
     d2 = dict(d, cu_seqlens_q=tuple(new_cq))
-    q = np.concatenate([w.slice(W.TENSOR_Q, a, b, heads=hs).double().numpy() for a, b in rows])
-    do = np.concatenate([w.slice(W.TENSOR_DO, a, b, heads=hs).double().numpy() for a, b in rows])
-    k = w.slice(W.TENSOR_K, 0, w.total_k, heads=hs).double().numpy()
-    v = w.slice(W.TENSOR_V, 0, w.total_k, heads=hs).double().numpy()
     pairs = 0
     for s in range(w.num_segments):
         lq = new_cq[s + 1] - new_cq[s]
         for j in range(w.kv_first[s], w.kv_first[s] + w.kv_count[s]):
             pairs += lq * (w.cu_seqlens_k[j + 1] - w.cu_seqlens_k[j])
-    t0 = time.perf_counter()
-    fwd = oracle.packed_forward(d2, q, k, v, w.scale)
-    for s in range(w.num_segments):
-        if w.kind[s] == W.SHARD:
-            a, b = new_cq[s], new_cq[s + 1]
-            for h in range(len(hs)):
-                oracle.lse_merge(fwd["o_part"][:, a:b, h], fwd["lse_part"][:, a:b, h])
-    oracle.packed_backward(d2, q, k, v, do, w.scale)
-    dt = time.perf_counter() - t0
-    flops = 14.0 * w.head_dim * len(hs) * pairs
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{len(hs)} of {w.num_heads} heads; whole segments in full, each shard's first 1/9 of "
-                      f"query rows against all blocks; fwd+merge+bwd fp64; {pairs} pairs/head, {dt:.1f} s"}
+    spent, heads = 0.0, 0
+    while heads < w.num_heads and spent < min_seconds:
+        hs = [heads]
+        q = np.concatenate([w.slice(W.TENSOR_Q, a, b, heads=hs).double().numpy() for a, b in rows])
+        do = np.concatenate([w.slice(W.TENSOR_DO, a, b, heads=hs).double().numpy() for a, b in rows])
+        k = w.slice(W.TENSOR_K, 0, w.total_k, heads=hs).double().numpy()
+        v = w.slice(W.TENSOR_V, 0, w.total_k, heads=hs).double().numpy()
+        t0 = time.perf_counter()
+        fwd = oracle.packed_forward(d2, q, k, v, w.scale)
+        for s in range(w.num_segments):
+            if w.kind[s] == W.SHARD:
+                a, b = new_cq[s], new_cq[s + 1]
+                oracle.lse_merge(fwd["o_part"][:, a:b, 0], fwd["lse_part"][:, a:b, 0])
+        oracle.packed_backward(d2, q, k, v, do, w.scale)
+        spent += time.perf_counter() - t0
+        heads += 1
+    flops = 14.0 * w.head_dim * heads * pairs
+    return {"value": flops / spent / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{heads} of {w.num_heads} heads; whole segments in full, each shard's first 1/9 of "
+                      f"query rows against all blocks; fwd+merge+bwd fp64; {pairs} pairs/head, {spent:.1f} s"}
 
 
 def main():
@@ -192,7 +196,7 @@ def main():
         rec["merge_kernel"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": mbytes}
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_heads)
+        rec["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(rec), flush=True)
 
 
