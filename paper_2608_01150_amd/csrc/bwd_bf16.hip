@@ -112,12 +112,14 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
       qreg[r] = ok ? *reinterpret_cast<const u32x4*>(qb_ + r * RSTEP * rs) : u32x4{0, 0, 0, 0};
       oreg[r] = ok ? *reinterpret_cast<const u32x4*>(ob_ + r * RSTEP * rs) : u32x4{0, 0, 0, 0};
     }
-    if (tid < BQ) {
-      // rows past the segment: LSE = +big makes P = 0 there
-      sreg = tid < nq ? lseg[(int64_t)(q0 + tid) * H] * 1.4426950408889634f : 1.0e30f;
-    } else if (tid < 2 * BQ) {
-      sreg = tid - BQ < nq ? dsg[(int64_t)(q0 + tid - BQ) * H] : 0.f;
-    }
+    // threads [0, BQ) stage LSE (log2 units), [BQ, 2BQ) stage D; the load
+    // address is clamped into the segment so it is always valid, and rows
+    // past the segment get LSE = +big (P = 0 there) and D = 0.
+    const int r = tid & (BQ - 1);
+    const int rc = min(q0 + r, it.q_len - 1);
+    const bool is_lse = tid < BQ;
+    const float x = is_lse ? lseg[(int64_t)rc * H] : dsg[(int64_t)rc * H];
+    sreg = r < nq ? (is_lse ? x * 1.4426950408889634f : x) : (is_lse ? 1.0e30f : 0.f);
   };
   auto stash = [&](int buf) {
 #pragma unroll
@@ -125,8 +127,7 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
       *reinterpret_cast<u32x4*>(qs[buf] + st_off + r * RSTEP * PITCH) = qreg[r];
       *reinterpret_cast<u32x4*>(dos[buf] + st_off + r * RSTEP * PITCH) = oreg[r];
     }
-    if (tid < BQ) lse2s[buf][tid] = sreg;
-    else if (tid < 2 * BQ) dsums[buf][tid - BQ] = sreg;
+    if (tid < 2 * BQ) (tid < BQ ? lse2s[buf] : dsums[buf])[tid & (BQ - 1)] = sreg;
   };
 
   fetch(0);
@@ -134,8 +135,10 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   int buf = 0;
   for (int q0 = 0; q0 < it.q_len; q0 += BQ, buf ^= 1) {
     __syncthreads();  // tile `buf` is complete; tile buf^1 is no longer read
-    const bool more = q0 + BQ < it.q_len;
-    if (more) fetch(q0 + BQ);
+    // Fetch the next tile unconditionally: past the segment it is all zero
+    // fills (no loads), and keeping the loop body free of branches keeps the
+    // dK/dV accumulators in place.
+    fetch(q0 + BQ);
     const char* qa = qs[buf] + a_off;
     const char* oa = dos[buf] + a_off;
     const char* qt = qs[buf] + t_off;
@@ -165,7 +168,8 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
             const int tt = 2 * t + e, i = 8 * h + tt;
             const float l2 = tt < 4 ? l0[tt] : l1[tt - 4];
             const float dd = tt < 4 ? d0[tt] : d1[tt - 4];
-            const float pr = k_ok ? fast_exp2(fmaf(s[i], p.scale_log2, -l2)) : 0.f;
+            // A key past the range (k_ok false) only feeds its own dK/dV, never stored.
+            const float pr = fast_exp2(fmaf(s[i], p.scale_log2, -l2));
             pv[e] = pr;
             dsv[e] = pr * (dp[i] - dd);
           }
@@ -182,8 +186,10 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
           dk[db] = mfma32(tr_operand<D>(qt, sb * 32 + 16 * h, db * 32), pds[h], dk[db]);
         }
       }
+      // keep the next sub-block's loads from being hoisted across this one
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (more) stash(buf ^ 1);
+    stash(buf ^ 1);
   }
 
   // dK = scale * dK^T, dV = dV^T: register i <-> d = db*32 + 16*(i/8) + 8g + i%8, key = lane's key.
@@ -309,17 +315,16 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
         dp = mfma32(*reinterpret_cast<const u32x4*>(va + poff<D>(kb * 32, kk * 16)), of[kk], dp);
       }
       // register i <-> key kb*32 + 16*(i/8) + 8g + i%8 of this tile, query = lane's row
+      float e[16];
 #pragma unroll
-      for (int i = 0; i < 16; i += 2) {
-        float e[2];
+      for (int i = 0; i < 16; ++i) e[i] = fast_exp2(fmaf(s[i], p.scale_log2, -lse2)) * (dp[i] - dd);
+      if (nvalid < BN) {  // partial last tile of a range: keys past it contribute nothing
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int keyi = kb * 32 + 16 * ((i + u) >> 3) + 8 * g + ((i + u) & 7);
-          const float pr = fast_exp2(fmaf(s[i + u], p.scale_log2, -lse2));
-          e[u] = (nvalid >= BN || keyi < nvalid) ? pr * (dp[i + u] - dd) : 0.f;
-        }
-        pds[kb][i >> 3][(i & 7) >> 1] = pack_bf16(e[0], e[1]);
+        for (int i = 0; i < 16; ++i)
+          if (kb * 32 + 16 * (i >> 3) + 8 * g + (i & 7) >= nvalid) e[i] = 0.f;
       }
+#pragma unroll
+      for (int i = 0; i < 16; i += 2) pds[kb][i >> 3][(i & 7) >> 1] = pack_bf16(e[i], e[i + 1]);
     }
     // dQ^T[d, q] += sum_key K^T[d, key] dS^T[key, q]; A row m <-> d = db*32 + perm32(m).
 #pragma unroll
