@@ -58,13 +58,10 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   constexpr int BQ = kBwdTileM;                 // 64 queries per step
   constexpr int PITCH = Pad<D>::PITCH;
   constexpr int TILE = BQ * PITCH;              // bytes of one Q (or dO) tile
-  constexpr int CPR = D / 8;                    // 16-byte chunks per row
-  constexpr int CH = BQ * CPR / NT;             // chunks per thread per tile
-  constexpr int RSTEP = NT / CPR;
-  __shared__ __attribute__((aligned(16))) char qs[2][TILE];
-  __shared__ __attribute__((aligned(16))) char dos[2][TILE];
-  __shared__ __attribute__((aligned(16))) float lse2s[2][BQ];
-  __shared__ __attribute__((aligned(16))) float dsums[2][BQ];
+  // Two buffers of each tile as separate objects, so the compiler can tell the
+  // direct-to-LDS loads filling one buffer from the reads of the other.
+  __shared__ __attribute__((aligned(16))) char qs0[TILE], qs1[TILE], dos0[TILE], dos1[TILE];
+  __shared__ __attribute__((aligned(16))) float lse0[BQ], lse1[BQ], dsm0[BQ], dsm1[BQ];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ln = lane & 31, g = lane >> 5;
@@ -94,72 +91,59 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
     dv[db] = f32x16{};
   }
 
-  const int srow = tid / CPR, scol = tid % CPR;
-  const uint32_t st_off = poff<D>(srow, scol * 8);
   const uint32_t a_off = poff<D>(perm32(ln), g * 8);
   const uint32_t t_off = tr_lane_off<D>(lane);
-  const int64_t g_off = srow * rs + scol * 8;
 
-  u32x4 qreg[CH], oreg[CH];
-  float sreg = 0.f;
-  auto fetch = [&](int q0) {
-    const int nq = it.q_len - q0;
-    const uint16_t* qb_ = qg + q0 * rs + g_off;
-    const uint16_t* ob_ = dog + q0 * rs + g_off;
-#pragma unroll
-    for (int r = 0; r < CH; ++r) {
-      const bool ok = srow + r * RSTEP < nq;
-      qreg[r] = ok ? *reinterpret_cast<const u32x4*>(qb_ + r * RSTEP * rs) : u32x4{0, 0, 0, 0};
-      oreg[r] = ok ? *reinterpret_cast<const u32x4*>(ob_ + r * RSTEP * rs) : u32x4{0, 0, 0, 0};
-    }
-    // threads [0, BQ) stage LSE (log2 units), [BQ, 2BQ) stage D; the load
-    // address is clamped into the segment so it is always valid, and rows
-    // past the segment get LSE = +big (P = 0 there) and D = 0.
+  // Q/dO tiles go straight to LDS; LSE (log2 units) and D are staged through
+  // one register per thread: threads [0, BQ) LSE, [BQ, 2BQ) D.  Loads are
+  // clamped into the segment, and rows past it get LSE = +big (P = 0 there)
+  // and D = 0.
+  // The raw value is only consumed at stash time: vmcnt is in order, so an
+  // early use would also wait for every tile load issued before it.
+  float sraw = 0.f;
+  bool sok = false;
+  const bool is_lse = tid < BQ;
+  auto fetch = [&](int q0, char* qdst, char* odst) {
+    const int nq = it.q_len - q0;  // >= 1: q0 is clamped into the segment
     const int r = tid & (BQ - 1);
     const int rc = min(q0 + r, it.q_len - 1);
-    const bool is_lse = tid < BQ;
-    const float x = is_lse ? lseg[(int64_t)rc * H] : dsg[(int64_t)rc * H];
-    sreg = r < nq ? (is_lse ? x * 1.4426950408889634f : x) : (is_lse ? 1.0e30f : 0.f);
+    sraw = is_lse ? lseg[(int64_t)rc * H] : dsg[(int64_t)rc * H];
+    sok = r < nq;
+    dma_tile<D, BQ>(qdst, qg + q0 * rs, rs, nq, wave, lane);
+    dma_tile<D, BQ>(odst, dog + q0 * rs, rs, nq, wave, lane);
   };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int r = 0; r < CH; ++r) {
-      *reinterpret_cast<u32x4*>(qs[buf] + st_off + r * RSTEP * PITCH) = qreg[r];
-      *reinterpret_cast<u32x4*>(dos[buf] + st_off + r * RSTEP * PITCH) = oreg[r];
-    }
-    if (tid < 2 * BQ) (tid < BQ ? lse2s[buf] : dsums[buf])[tid & (BQ - 1)] = sreg;
+  auto stash = [&](float* ldst, float* ddst) {
+    wait_vmem();
+    const float x = sok ? (is_lse ? sraw * 1.4426950408889634f : sraw) : (is_lse ? 1.0e30f : 0.f);
+    if (tid < 2 * BQ) (is_lse ? ldst : ddst)[tid & (BQ - 1)] = x;
   };
 
-  fetch(0);
-  stash(0);
-  int buf = 0;
-  for (int q0 = 0; q0 < it.q_len; q0 += BQ, buf ^= 1) {
-    __syncthreads();  // tile `buf` is complete; tile buf^1 is no longer read
-    // Fetch the next tile unconditionally: past the segment it is all zero
-    // fills (no loads), and keeping the loop body free of branches keeps the
-    // dK/dV accumulators in place.
-    fetch(q0 + BQ);
-    const char* qa = qs[buf] + a_off;
-    const char* oa = dos[buf] + a_off;
-    const char* qt = qs[buf] + t_off;
-    const char* ot = dos[buf] + t_off;
-#pragma unroll
-    for (int sb = 0; sb < BQ / 32; ++sb) {
-      // S and dP: D row m <-> query sb*32 + perm32(m); register i <-> query sb*32 + 16*(i/8) + 8g + i%8.
-      f32x16 s = f32x16{}, dp = f32x16{};
+  // One 64-query step on the tiles (qt_, ot_, ls, ds).
+  auto step = [&](const char* qbuf, const char* obuf, const float* ls, const float* ds) {
+    const char* qa = qbuf + a_off;
+    const char* oa = obuf + a_off;
+    const char* qt = qbuf + t_off;
+    const char* ot = obuf + t_off;
+    // S and dP of sub-block sb (32 queries): D row m <-> query sb*32 +
+    // perm32(m); register i <-> query sb*32 + 16*(i/8) + 8g + i%8.
+    auto sdp = [&](int sb, f32x16& s, f32x16& dp) {
+      s = f32x16{};
+      dp = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) {
         s = mfma32(*reinterpret_cast<const u32x4*>(qa + poff<D>(sb * 32, kk * 16)), kf[kk], s);
         dp = mfma32(*reinterpret_cast<const u32x4*>(oa + poff<D>(sb * 32, kk * 16)), vf[kk], dp);
       }
-      u32x4 pp[2], pds[2];
+    };
+    // P = exp(S - LSE), dS = P (dP - D), packed as bf16 B operands (k = queries).
+    auto softmax = [&](int sb, const f32x16& s, const f32x16& dp, u32x4* pp, u32x4* pds) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int q8 = sb * 32 + 16 * h + 8 * g;
-        const f32x4 l0 = *reinterpret_cast<const f32x4*>(&lse2s[buf][q8]);
-        const f32x4 l1 = *reinterpret_cast<const f32x4*>(&lse2s[buf][q8 + 4]);
-        const f32x4 d0 = *reinterpret_cast<const f32x4*>(&dsums[buf][q8]);
-        const f32x4 d1 = *reinterpret_cast<const f32x4*>(&dsums[buf][q8 + 4]);
+        const f32x4 l0 = *reinterpret_cast<const f32x4*>(&ls[q8]);
+        const f32x4 l1 = *reinterpret_cast<const f32x4*>(&ls[q8 + 4]);
+        const f32x4 d0 = *reinterpret_cast<const f32x4*>(&ds[q8]);
+        const f32x4 d1 = *reinterpret_cast<const f32x4*>(&ds[q8 + 4]);
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           float pv[2], dsv[2];
@@ -177,7 +161,9 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
           pds[h][t] = pack_bf16(dsv[0], dsv[1]);
         }
       }
-      // dV^T += dO^T P and dK^T += Q^T dS; A row m <-> d = db*32 + perm32(m), k <-> queries.
+    };
+    // dV^T += dO^T P and dK^T += Q^T dS; A row m <-> d = db*32 + perm32(m), k <-> queries.
+    auto dvdk = [&](int sb, const u32x4* pp, const u32x4* pds) {
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
@@ -186,10 +172,53 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
           dk[db] = mfma32(tr_operand<D>(qt, sb * 32 + 16 * h, db * 32), pds[h], dk[db]);
         }
       }
-      // keep the next sub-block's loads from being hoisted across this one
-      __builtin_amdgcn_sched_barrier(0);
+    };
+    // Two-stage pipeline over the two sub-blocks: the MFMAs of one stage are
+    // interleaved with the softmax VALU work of the other.
+    f32x16 s0, dp0, s1, dp1;
+    u32x4 pp0[2], pds0[2], pp1[2], pds1[2];
+    sdp(0, s0, dp0);
+    __builtin_amdgcn_sched_barrier(0);
+    sdp(1, s1, dp1);
+    softmax(0, s0, dp0, pp0, pds0);
+#pragma unroll
+    for (int i = 0; i < D / 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // five VALU
     }
-    stash(buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+    dvdk(0, pp0, pds0);
+    softmax(1, s1, dp1, pp1, pds1);
+#pragma unroll
+    for (int i = 0; i < D / 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);  // two LDS reads (one transposed operand)
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 1);  // five VALU
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    dvdk(1, pp1, pds1);
+  };
+
+  // Ping-pong over the two buffer sets, unrolled by two so each half names
+  // its buffers statically.  The next tile is fetched unconditionally (past
+  // the segment it reloads the last row, never read as data): the loop body
+  // stays free of branches, which keeps the dK/dV accumulators in place.
+  fetch(0, qs0, dos0);
+  stash(lse0, dsm0);
+  for (int q0 = 0;;) {
+    __syncthreads();  // buffers 0 complete; buffers 1 no longer read
+    fetch(min(q0 + BQ, it.q_len - 1), qs1, dos1);
+    step(qs0, dos0, lse0, dsm0);
+    stash(lse1, dsm1);
+    q0 += BQ;
+    if (q0 >= it.q_len) break;
+    __syncthreads();  // buffers 1 complete; buffers 0 no longer read
+    fetch(min(q0 + BQ, it.q_len - 1), qs0, dos0);
+    step(qs1, dos1, lse1, dsm1);
+    stash(lse0, dsm0);
+    q0 += BQ;
+    if (q0 >= it.q_len) break;
   }
 
   // dK = scale * dK^T, dV = dV^T: register i <-> d = db*32 + 16*(i/8) + 8g + i%8, key = lane's key.

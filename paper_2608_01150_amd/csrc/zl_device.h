@@ -61,6 +61,35 @@ __device__ __forceinline__ constexpr uint32_t poff(int row, int col) {
   return row * Pad<D>::PITCH + col * 2;
 }
 
+// Stage rows [0, ROWS) of one head of a packed [T, H, D] bf16 tensor (row 0
+// at g_row0, `rs` elements between rows) into a padded LDS tile with direct
+// global->LDS 16-byte loads (global_load_lds_dwordx4: lane l of a wave lands
+// at the wave-uniform base + 16*l).  A 64-row tile is a whole number of
+// 64-slot wave instructions (19 of them for D = 128, 9 for D = 64); each of
+// the 4 waves issues ceil(NJ/4) of them, the surplus ones clamped onto the
+// last block (rewriting identical bytes), so there is no branch.  Padding
+// slots reload chunk 0 of their row, and rows at or past `nvalid` (>= 1)
+// reload row nvalid-1: finite data the callers mask.  Completion is tracked
+// by vmcnt; callers wait before the barrier that publishes the tile.
+template <int D, int ROWS>
+__device__ __forceinline__ void dma_tile(char* tile, const uint16_t* g_row0, int64_t rs, int nvalid, int wave,
+                                         int lane) {
+  constexpr int SPR = Pad<D>::PITCH / 16;
+  constexpr int NJ = ROWS * SPR / 64;
+  static_assert(ROWS * SPR % 64 == 0, "tile must be whole wave instructions");
+#pragma unroll
+  for (int jj = 0; jj < (NJ + 3) / 4; ++jj) {
+    const int j = min(wave + 4 * jj, NJ - 1);
+    const int slot = j * 64 + lane;
+    const int row = slot / SPR, chunk = slot % SPR;
+    const int rr = min(row, nvalid - 1);
+    const int cc = chunk < D / 8 ? chunk : 0;
+    __builtin_amdgcn_global_load_lds(g_row0 + rr * rs + cc * 8, tile + j * 1024, 16, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 // LDS transpose read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
