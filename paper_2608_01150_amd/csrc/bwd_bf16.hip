@@ -18,8 +18,8 @@
 //                    dQ^T += K^T dS^T                 MFMA
 //                  A shard row sums its blocks inside one item.
 // Q/dO (dK/dV) and K/V (dQ) tiles are staged row-major (padded pitch,
-// conflict-free) in double-buffered LDS, the next tile fetched into registers
-// while the current one computes; the transposed operands (Q^T, dO^T, K^T)
+// conflict-free) in double-buffered LDS by direct global-to-LDS loads issued
+// while the previous tile computes; the transposed operands (Q^T, dO^T, K^T)
 // come straight from the row-major tiles through LDS transpose reads.
 
 #include <algorithm>
@@ -247,11 +247,8 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
   constexpr int BN = kDqTileN;                  // 64 keys per step
   constexpr int PITCH = Pad<D>::PITCH;
   constexpr int TILE = BN * PITCH;
-  constexpr int CPR = D / 8;
-  constexpr int CH = BN * CPR / NT;
-  constexpr int RSTEP = NT / CPR;
-  __shared__ __attribute__((aligned(16))) char ks[2][TILE];
-  __shared__ __attribute__((aligned(16))) char vs[2][TILE];
+  // Two buffers of each tile as separate objects (see the dK/dV kernel).
+  __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], vs0[TILE], vs1[TILE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ln = lane & 31, g = lane >> 5;
@@ -278,16 +275,13 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) dq[db] = f32x16{};
 
-  const int srow = tid / CPR, scol = tid % CPR;
-  const uint32_t st_off = poff<D>(srow, scol * 8);
   const uint32_t a_off = poff<D>(perm32(ln), g * 8);
   const uint32_t t_off = tr_lane_off<D>(lane);
-  const int64_t g_off = srow * rs + scol * 8;
 
   // Key tiles run over the segment's ranges in order; (r, kt) is the tile
   // [cu_k[r] + kt, cu_k[r] + kt + BN) clipped to the range.
   const int r_end = sr.kv_first + sr.kv_count;
-  auto first_tile = [&](int r, int kt, int* ro, int* kto) {
+  auto next_tile = [&](int r, int kt, int* ro, int* kto) {
     while (r < r_end && kt >= p.cu_k[r + 1] - p.cu_k[r]) {
       ++r;
       kt = 0;
@@ -295,44 +289,18 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
     *ro = r;
     *kto = kt;
   };
-  u32x4 kreg[CH], vreg[CH];
-  auto fetch = [&](int r, int kt) {
+  auto fetch = [&](int r, int kt, char* kdst, char* vdst) {
     const int k0 = p.cu_k[r] + kt, nvalid = p.cu_k[r + 1] - k0;
-    const uint16_t* kb_ = static_cast<const uint16_t*>(p.k) + ((int64_t)k0 * H + it.head) * D + g_off;
-    const uint16_t* vb_ = static_cast<const uint16_t*>(p.v) + ((int64_t)k0 * H + it.head) * D + g_off;
-#pragma unroll
-    for (int c8 = 0; c8 < CH; ++c8) {
-      const bool ok = srow + c8 * RSTEP < nvalid;
-      kreg[c8] = ok ? *reinterpret_cast<const u32x4*>(kb_ + c8 * RSTEP * rs) : u32x4{0, 0, 0, 0};
-      vreg[c8] = ok ? *reinterpret_cast<const u32x4*>(vb_ + c8 * RSTEP * rs) : u32x4{0, 0, 0, 0};
-    }
-  };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int c8 = 0; c8 < CH; ++c8) {
-      *reinterpret_cast<u32x4*>(ks[buf] + st_off + c8 * RSTEP * PITCH) = kreg[c8];
-      *reinterpret_cast<u32x4*>(vs[buf] + st_off + c8 * RSTEP * PITCH) = vreg[c8];
-    }
+    const uint16_t* kb_ = static_cast<const uint16_t*>(p.k) + ((int64_t)k0 * H + it.head) * D;
+    const uint16_t* vb_ = static_cast<const uint16_t*>(p.v) + ((int64_t)k0 * H + it.head) * D;
+    dma_tile<D, BN>(kdst, kb_, rs, nvalid, wave, lane);
+    dma_tile<D, BN>(vdst, vb_, rs, nvalid, wave, lane);
   };
 
-  int r, kt;
-  first_tile(sr.kv_first, 0, &r, &kt);
-  if (r < r_end) {
-    fetch(r, kt);
-    stash(0);
-  }
-  int buf = 0;
-  while (r < r_end) {
-    __syncthreads();  // tile `buf` complete; buf^1 free
-    const int nvalid = p.cu_k[r + 1] - p.cu_k[r] - kt;
-    int rn, ktn;
-    first_tile(r, kt + BN, &rn, &ktn);
-    const bool more = rn < r_end;
-    if (more) fetch(rn, ktn);
-    const char* ka = ks[buf] + a_off;
-    const char* va = vs[buf] + a_off;
-    const char* kt_ = ks[buf] + t_off;
-
+  auto step = [&](const char* kbuf, const char* vbuf, int nvalid) {
+    const char* ka = kbuf + a_off;
+    const char* va = vbuf + a_off;
+    const char* kt_ = kbuf + t_off;
     // S^T and dP^T for keys [kb*32, kb*32+32): D row m <-> key kb*32 + perm32(m).
     u32x4 pds[2][2];
 #pragma unroll
@@ -365,10 +333,37 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
           dq[db] = mfma32(tr_operand<D>(kt_, kb * 32 + 16 * s2, db * 32), pds[kb][s2], dq[db]);
       }
     }
-    if (more) stash(buf ^ 1);
-    buf ^= 1;
-    r = rn;
-    kt = ktn;
+  };
+
+  // Ping-pong over the two buffer sets, unrolled by two.  The next tile is
+  // fetched unconditionally: after the last one the current tile is reloaded
+  // into the idle buffer (never read).
+  int r, kt;
+  next_tile(sr.kv_first, 0, &r, &kt);
+  if (r < r_end) {
+    fetch(r, kt, ks0, vs0);
+    wait_vmem();
+    for (;;) {
+      int rn, ktn;
+      __syncthreads();  // buffers 0 complete; buffers 1 no longer read
+      next_tile(r, kt + BN, &rn, &ktn);
+      bool more = rn < r_end;
+      fetch(more ? rn : r, more ? ktn : kt, ks1, vs1);
+      step(ks0, vs0, p.cu_k[r + 1] - p.cu_k[r] - kt);
+      wait_vmem();
+      if (!more) break;
+      r = rn;
+      kt = ktn;
+      __syncthreads();  // buffers 1 complete; buffers 0 no longer read
+      next_tile(r, kt + BN, &rn, &ktn);
+      more = rn < r_end;
+      fetch(more ? rn : r, more ? ktn : kt, ks0, vs0);
+      step(ks1, vs1, p.cu_k[r + 1] - p.cu_k[r] - kt);
+      wait_vmem();
+      if (!more) break;
+      r = rn;
+      kt = ktn;
+    }
   }
 
   // dq[db][i] is (d = db*32 + 16*(i/8) + 8g + i%8, query qr).

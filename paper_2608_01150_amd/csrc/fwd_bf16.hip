@@ -11,8 +11,8 @@
 // Computing the transposed products keeps one query per lane, so the row max
 // needs a single cross-lane exchange (lanes l and l^32) and the softmax
 // output is already the B operand of the next MFMA.  K and V tiles are staged
-// row-major (padded pitch, conflict-free) in double-buffered LDS; the next
-// tile is fetched into registers while the current one computes, one barrier
+// row-major (padded pitch, conflict-free) in double-buffered LDS by direct
+// global-to-LDS loads issued while the previous tile computes, one barrier
 // per step.
 //
 // Epilogue: WHOLE items write the final bf16 output and the LSE; SHARD items
@@ -36,11 +36,9 @@ template <int D>
 __global__ __launch_bounds__(NT, 2) void fwd_bf16_kernel(FwdParams p) {
   constexpr int PITCH = Pad<D>::PITCH;
   constexpr int TILE = BN * PITCH;
-  constexpr int CPR = D / 8;           // 16-byte chunks per row
-  constexpr int CH = BN * CPR / NT;    // chunks per thread per tile
-  constexpr int RSTEP = NT / CPR;      // rows between a thread's chunks
-  __shared__ __attribute__((aligned(16))) char ks[2][TILE];
-  __shared__ __attribute__((aligned(16))) char vs[2][TILE];
+  // Two buffers of each tile as separate objects, so the compiler can tell the
+  // direct-to-LDS loads filling one buffer from the reads of the other.
+  __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], vs0[TILE], vs1[TILE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ln = lane & 31, g = lane >> 5;
@@ -63,45 +61,21 @@ __global__ __launch_bounds__(NT, 2) void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) o[db] = f32x16{};
 
-  // Per-lane LDS offsets: staging chunk, A-operand row perm32(ln), transpose piece.
-  const int srow = tid / CPR, scol = tid % CPR;
-  const uint32_t st_off = poff<D>(srow, scol * 8);
+  // Per-lane LDS offsets: A-operand row perm32(ln), transpose piece.
   const uint32_t a_off = poff<D>(perm32(ln), g * 8);
   const uint32_t t_off = tr_lane_off<D>(lane);
-  const int64_t g_off = srow * rs + scol * 8;
 
-  u32x4 kreg[CH], vreg[CH];
-  auto fetch = [&](int kt) {
+  // K/V tile starting at key kt (clamped into the range: rows past it reload
+  // the last key, masked below).
+  auto fetch = [&](int kt, char* kdst, char* vdst) {
     const int nvalid = it.k_len - kt;
-    const uint16_t* kb_ = kg + kt * rs + g_off;
-    const uint16_t* vb_ = vg + kt * rs + g_off;
-#pragma unroll
-    for (int r = 0; r < CH; ++r) {
-      const bool ok = srow + r * RSTEP < nvalid;
-      kreg[r] = ok ? *reinterpret_cast<const u32x4*>(kb_ + r * RSTEP * rs) : u32x4{0, 0, 0, 0};
-      vreg[r] = ok ? *reinterpret_cast<const u32x4*>(vb_ + r * RSTEP * rs) : u32x4{0, 0, 0, 0};
-    }
-  };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int r = 0; r < CH; ++r) {
-      *reinterpret_cast<u32x4*>(ks[buf] + st_off + r * RSTEP * PITCH) = kreg[r];
-      *reinterpret_cast<u32x4*>(vs[buf] + st_off + r * RSTEP * PITCH) = vreg[r];
-    }
+    dma_tile<D, BN>(kdst, kg + kt * rs, rs, nvalid, wave, lane);
+    dma_tile<D, BN>(vdst, vg + kt * rs, rs, nvalid, wave, lane);
   };
 
-  if (it.k_len > 0) {
-    fetch(0);
-    stash(0);
-  }
-  int buf = 0;
-  for (int kt = 0; kt < it.k_len; kt += BN, buf ^= 1) {
-    __syncthreads();  // tile `buf` is complete; tile buf^1 is no longer read
-    const bool more = kt + BN < it.k_len;
-    if (more) fetch(kt + BN);
-    const char* ka = ks[buf] + a_off;
-    const char* vt = vs[buf] + t_off;
-
+  auto step = [&](const char* kbuf, const char* vbuf, int kt) {
+    const char* ka = kbuf + a_off;
+    const char* vt = vbuf + t_off;
     // S^T for keys [kb*32, kb*32+32): D row m <-> key kb*32 + perm32(m).
     f32x16 s[2];
 #pragma unroll
@@ -164,7 +138,27 @@ __global__ __launch_bounds__(NT, 2) void fwd_bf16_kernel(FwdParams p) {
           o[db] = mfma32(tr_operand<D>(vt, kb * 32 + 16 * s2, db * 32), pb[kb][s2], o[db]);
       }
     }
-    if (more) stash(buf ^ 1);
+  };
+
+  // Ping-pong over the two buffer sets, unrolled by two; the next tile is
+  // fetched unconditionally (clamped into the range).
+  if (it.k_len > 0) {
+    fetch(0, ks0, vs0);
+    wait_vmem();
+    for (int kt = 0;;) {
+      __syncthreads();  // buffers 0 complete; buffers 1 no longer read
+      fetch(min(kt + BN, it.k_len - 1), ks1, vs1);
+      step(ks0, vs0, kt);
+      wait_vmem();
+      kt += BN;
+      if (kt >= it.k_len) break;
+      __syncthreads();  // buffers 1 complete; buffers 0 no longer read
+      fetch(min(kt + BN, it.k_len - 1), ks0, vs0);
+      step(ks1, vs1, kt);
+      wait_vmem();
+      kt += BN;
+      if (kt >= it.k_len) break;
+    }
   }
 
   // Epilogue.  o[db][i] is (d = db*32 + 16*(i/8) + 8*g + i%8, query qr).
