@@ -61,10 +61,27 @@ __device__ __forceinline__ constexpr uint32_t poff(int row, int col) {
   return row * Pad<D>::PITCH + col * 2;
 }
 
+// 32-bit LDS byte address of a pointer into a __shared__ object.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(size_t)((const __attribute__((address_space(3))) char*)p);
+}
+
+// One direct global->LDS 16-byte load per lane (global_load_lds_dwordx4): lane
+// l's 16 bytes land at the wave-uniform LDS address `lds` + 16*l.  Issued as
+// inline asm (M0 saved and restored around it) so that the compiler does not
+// treat it as an LDS store that every later LDS read must wait for; callers
+// wait for vmcnt themselves before the barrier that publishes the data.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  uint32_t save;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+               : "=&s"(save)
+               : "v"(g), "s"(lds)
+               : "memory");
+}
+
 // Stage rows [0, ROWS) of one head of a packed [T, H, D] bf16 tensor (row 0
 // at g_row0, `rs` elements between rows) into a padded LDS tile with direct
-// global->LDS 16-byte loads (global_load_lds_dwordx4: lane l of a wave lands
-// at the wave-uniform base + 16*l).  A 64-row tile is a whole number of
+// global->LDS 16-byte loads (dma16).  A 64-row tile is a whole number of
 // 64-slot wave instructions (19 of them for D = 128, 9 for D = 64); each of
 // the 4 waves issues ceil(NJ/4) of them, the surplus ones clamped onto the
 // last block (rewriting identical bytes), so there is no branch.  Padding
@@ -84,7 +101,7 @@ __device__ __forceinline__ void dma_tile(char* tile, const uint16_t* g_row0, int
     const int row = slot / SPR, chunk = slot % SPR;
     const int rr = min(row, nvalid - 1);
     const int cc = chunk < D / 8 ? chunk : 0;
-    __builtin_amdgcn_global_load_lds(g_row0 + rr * rs + cc * 8, tile + j * 1024, 16, 0, 0);
+    dma16(g_row0 + rr * rs + cc * 8, __builtin_amdgcn_readfirstlane(lds_addr(tile) + j * 1024));
   }
 }
 
