@@ -1,7 +1,8 @@
 // Packed whole+shard attention backward, bf16 inputs, gfx950 MFMA.
 //
 // Three launches on one stream, no atomics (results are deterministic):
-//   1. preprocess  D_i = dO_i . O_i in fp32 for every query row and head.
+//   1. preprocess  D_i = dO_i . O_i in fp32 for every query row and head, and
+//                  LSE_i in log2 units for the dK/dV kernel's staging.
 //   2. dK/dV       one workgroup per item = up to 128 keys (4 waves x 32) of one
 //                  head of one K/V range, looping over every query of the
 //                  owning segment in steps of 64 rows.  One key per lane:
@@ -49,7 +50,10 @@ __global__ __launch_bounds__(NT) void bwd_pre_kernel(BwdParams p) {
   }
 #pragma unroll
   for (int off = LPU / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if (live && sub == 0) p.dsum[u] = acc;
+  if (live && sub == 0) {
+    p.dsum[u] = acc;
+    p.lse2[u] = p.lse[u] * 1.4426950408889634f;
+  }
 }
 
 // ------------------------------------------------------------------ dK / dV
@@ -72,7 +76,6 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   const uint16_t* dog = static_cast<const uint16_t*>(p.dout) + ((int64_t)it.q_start * H + it.head) * D;
   const uint16_t* kg = static_cast<const uint16_t*>(p.k) + ((int64_t)it.k_start * H + it.head) * D;
   const uint16_t* vg = static_cast<const uint16_t*>(p.v) + ((int64_t)it.k_start * H + it.head) * D;
-  const float* lseg = p.lse + (int64_t)it.q_start * H + it.head;
   const float* dsg = p.dsum + (int64_t)it.q_start * H + it.head;
 
   // This lane's key (B-operand column) and its K, V fragments.
@@ -90,32 +93,26 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
     dk[db] = f32x16{};
     dv[db] = f32x16{};
   }
+  __builtin_amdgcn_s_waitcnt(0);  // prologue loads done (see the forward kernel)
 
   const uint32_t a_off = poff<D>(perm32(ln), g * 8);
   const uint32_t t_off = tr_lane_off<D>(lane);
 
-  // Q/dO tiles go straight to LDS; LSE (log2 units) and D are staged through
-  // one register per thread: threads [0, BQ) LSE, [BQ, 2BQ) D.  Loads are
-  // clamped into the segment, and rows past it get LSE = +big (P = 0 there)
-  // and D = 0.
-  // The raw value is only consumed at stash time: vmcnt is in order, so an
-  // early use would also wait for every tile load issued before it.
-  float sraw = 0.f;
-  bool sok = false;
-  const bool is_lse = tid < BQ;
-  auto fetch = [&](int q0, char* qdst, char* odst) {
+  // Q/dO tiles and the tile's LSE (log2 units) and D values go straight to
+  // LDS.  Q and dO rows past the segment read as zero, so they add exactly
+  // nothing to dK/dV (their P and dS stay finite: S = 0, dP = 0); their LSE
+  // and D entries repeat the last row.  The loop issues no register loads,
+  // so the compiler places no waits on the in-flight tile loads.
+  const float* l2g = p.lse2 + (int64_t)it.q_start * H + it.head;
+  auto fetch = [&](int q0, char* qdst, char* odst, float* ldst, float* ddst) {
     const int nq = it.q_len - q0;  // >= 1: q0 is clamped into the segment
-    const int r = tid & (BQ - 1);
-    const int rc = min(q0 + r, it.q_len - 1);
-    sraw = is_lse ? lseg[(int64_t)rc * H] : dsg[(int64_t)rc * H];
-    sok = r < nq;
-    dma_tile<D, BQ>(qdst, qg + q0 * rs, rs, nq, wave, lane);
-    dma_tile<D, BQ>(odst, dog + q0 * rs, rs, nq, wave, lane);
-  };
-  auto stash = [&](float* ldst, float* ddst) {
-    wait_vmem();
-    const float x = sok ? (is_lse ? sraw * 1.4426950408889634f : sraw) : (is_lse ? 1.0e30f : 0.f);
-    if (tid < 2 * BQ) (is_lse ? ldst : ddst)[tid & (BQ - 1)] = x;
+    dma_tile<D, BQ, true>(qdst, qg + q0 * rs, rs, nq, wave, lane);
+    dma_tile<D, BQ, true>(odst, dog + q0 * rs, rs, nq, wave, lane);
+    if (wave < 2) {
+      const int rc = min(q0 + lane, it.q_len - 1);
+      dma4((wave == 0 ? l2g : dsg) + (int64_t)rc * H,
+           __builtin_amdgcn_readfirstlane(lds_addr(wave == 0 ? ldst : ddst)));
+    }
   };
 
   // One 64-query step on the tiles (qt_, ot_, ls, ds).
@@ -204,19 +201,19 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   // its buffers statically.  The next tile is fetched unconditionally (past
   // the segment it reloads the last row, never read as data): the loop body
   // stays free of branches, which keeps the dK/dV accumulators in place.
-  fetch(0, qs0, dos0);
-  stash(lse0, dsm0);
+  fetch(0, qs0, dos0, lse0, dsm0);
+  wait_vmem();
   for (int q0 = 0;;) {
     __syncthreads();  // buffers 0 complete; buffers 1 no longer read
-    fetch(min(q0 + BQ, it.q_len - 1), qs1, dos1);
+    fetch(min(q0 + BQ, it.q_len - 1), qs1, dos1, lse1, dsm1);
     step(qs0, dos0, lse0, dsm0);
-    stash(lse1, dsm1);
+    wait_vmem();
     q0 += BQ;
     if (q0 >= it.q_len) break;
     __syncthreads();  // buffers 1 complete; buffers 0 no longer read
-    fetch(min(q0 + BQ, it.q_len - 1), qs0, dos0);
+    fetch(min(q0 + BQ, it.q_len - 1), qs0, dos0, lse0, dsm0);
     step(qs1, dos1, lse1, dsm1);
-    stash(lse0, dsm0);
+    wait_vmem();
     q0 += BQ;
     if (q0 >= it.q_len) break;
   }
@@ -274,6 +271,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
   f32x16 dq[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) dq[db] = f32x16{};
+  __builtin_amdgcn_s_waitcnt(0);  // prologue loads done (see the forward kernel)
 
   const uint32_t a_off = poff<D>(perm32(ln), g * 8);
   const uint32_t t_off = tr_lane_off<D>(lane);

@@ -56,6 +56,11 @@ __global__ __launch_bounds__(NT, 2) void fwd_bf16_kernel(FwdParams p) {
   for (int kk = 0; kk < D / 16; ++kk)
     qf[kk] = q_ok ? *reinterpret_cast<const u32x4*>(qg + qr * rs + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
 
+  // Wait for the prologue's register loads here, with a waitcnt the compiler
+  // sees: the step loop then carries no pending VGPR loads, so it inserts no
+  // vmcnt wait there (which would also drain the in-flight tile DMAs).
+  __builtin_amdgcn_s_waitcnt(0);
+
   float m_run = kNegBig, l_part = 0.f;
   f32x16 o[D / 32];
 #pragma unroll

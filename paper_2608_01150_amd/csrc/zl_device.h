@@ -79,16 +79,29 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
                : "memory");
 }
 
+// Same for 4 bytes per lane (global_load_lds_dword): lane l lands at lds + 4*l.
+__device__ __forceinline__ void dma4(const void* g, uint32_t lds) {
+  uint32_t save;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
+               : "=&s"(save)
+               : "v"(g), "s"(lds)
+               : "memory");
+}
+
+// 16 zero bytes in device memory: the source of tile rows that must read as zero.
+static __device__ __attribute__((aligned(16))) const uint32_t kZeroChunk[4] = {0u, 0u, 0u, 0u};
+
 // Stage rows [0, ROWS) of one head of a packed [T, H, D] bf16 tensor (row 0
 // at g_row0, `rs` elements between rows) into a padded LDS tile with direct
 // global->LDS 16-byte loads (dma16).  A 64-row tile is a whole number of
 // 64-slot wave instructions (19 of them for D = 128, 9 for D = 64); each of
 // the 4 waves issues ceil(NJ/4) of them, the surplus ones clamped onto the
 // last block (rewriting identical bytes), so there is no branch.  Padding
-// slots reload chunk 0 of their row, and rows at or past `nvalid` (>= 1)
-// reload row nvalid-1: finite data the callers mask.  Completion is tracked
-// by vmcnt; callers wait before the barrier that publishes the tile.
-template <int D, int ROWS>
+// slots reload chunk 0 of their row.  Rows at or past `nvalid` (>= 1) reload
+// row nvalid-1 (finite data the caller masks) or, with ZERO_TAIL, read as
+// zero.  Completion is tracked by vmcnt; callers wait before the barrier that
+// publishes the tile.
+template <int D, int ROWS, bool ZERO_TAIL = false>
 __device__ __forceinline__ void dma_tile(char* tile, const uint16_t* g_row0, int64_t rs, int nvalid, int wave,
                                          int lane) {
   constexpr int SPR = Pad<D>::PITCH / 16;
@@ -101,7 +114,9 @@ __device__ __forceinline__ void dma_tile(char* tile, const uint16_t* g_row0, int
     const int row = slot / SPR, chunk = slot % SPR;
     const int rr = min(row, nvalid - 1);
     const int cc = chunk < D / 8 ? chunk : 0;
-    dma16(g_row0 + rr * rs + cc * 8, __builtin_amdgcn_readfirstlane(lds_addr(tile) + j * 1024));
+    const void* src = g_row0 + rr * rs + cc * 8;
+    if (ZERO_TAIL && row >= nvalid) src = kZeroChunk;
+    dma16(src, __builtin_amdgcn_readfirstlane(lds_addr(tile) + j * 1024));
   }
 }
 

@@ -18,6 +18,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <list>
 #include <mutex>
@@ -362,6 +363,17 @@ hipError_t timed(int kid, hipStream_t s, F&& launch) {
   return e;
 }
 
+// Work items per XCD run of the dispatch order (see dispatch_item): read
+// once from ZL_XCD_CHUNK, default 1 (plain hardware order).
+int32_t xcd_chunk() {
+  static const int32_t v = [] {
+    const char* e = std::getenv("ZL_XCD_CHUNK");
+    const long x = e ? std::strtol(e, nullptr, 10) : 1;
+    return (int32_t)(x >= 1 && x <= 4096 ? x : 1);
+  }();
+  return v;
+}
+
 zl_status hip_status(hipError_t e, const char* what) {
   if (e == hipSuccess) return ok();
   return fail(ZL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -387,7 +399,7 @@ zl_status zl_workspace_size(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_d
     return ok();
   }
   if (op != ZL_OP_BWD) return fail(ZL_ERR_INVALID_ARG, "op must be ZL_OP_FWD or ZL_OP_BWD");
-  *bytes = align256((size_t)sh.total_q * H * sizeof(float));
+  *bytes = 2 * align256((size_t)sh.total_q * H * sizeof(float));
   return ok();
 }
 
@@ -428,7 +440,7 @@ zl_status zl_attn_fwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype d
   p.lse_slot_stride = (int64_t)sh.total_q * H;
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
-  p.xcd_chunk = 1;
+  p.xcd_chunk = xcd_chunk();
   hipError_t e = timed(ZL_K_FWD, s, [&] {
     return dt == ZL_BF16 ? zl::launch_fwd_bf16(p, hd, s) : zl::launch_fwd_fp32(p, hd, s);
   });
@@ -506,6 +518,7 @@ zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype d
   p.dk = dk;
   p.dv = dv;
   p.dsum = static_cast<float*>(workspace);
+  p.lse2 = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256((size_t)sh.total_q * H * sizeof(float)));
   const char* base = static_cast<const char*>(plan->dev);
   p.kv_items = reinterpret_cast<const zl::Item*>(base);
   p.n_kv_items = plan->n_items;
@@ -517,7 +530,7 @@ zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype d
   p.total_q = sh.total_q;
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
-  p.xcd_chunk = 1;
+  p.xcd_chunk = xcd_chunk();
   hipError_t e = timed(ZL_K_BWD_PRE, s, [&] { return zl::launch_bwd_bf16(p, hd, 0, s); });
   if (e == hipSuccess) e = timed(ZL_K_BWD_DKDV, s, [&] { return zl::launch_bwd_bf16(p, hd, 1, s); });
   if (e == hipSuccess) e = timed(ZL_K_BWD_DQ, s, [&] { return zl::launch_bwd_bf16(p, hd, 2, s); });

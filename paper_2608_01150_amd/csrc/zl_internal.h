@@ -96,6 +96,7 @@ struct BwdParams {
   void* dk;
   void* dv;
   float* dsum;                 // [Tq, H] fp32 workspace: D = rowsum(dO * O)
+  float* lse2;                 // [Tq, H] fp32 workspace: LSE * log2(e)
   const Item* kv_items;        // dK/dV items: one key tile against all of its segment's queries
   int32_t n_kv_items;
   const Item* q_items;         // dQ items: one query tile against every key of its segment
