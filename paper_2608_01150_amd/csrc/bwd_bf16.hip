@@ -67,7 +67,8 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   __shared__ __attribute__((aligned(16))) char qs0[TILE], qs1[TILE], dos0[TILE], dos1[TILE];
   __shared__ __attribute__((aligned(16))) float lse0[BQ], lse1[BQ], dsm0[BQ], dsm1[BQ];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ln = lane & 31, g = lane >> 5;
   const Item it = p.kv_items[dispatch_item(blockIdx.x, p.n_kv_items, p.xcd_chunk)];
   const int H = p.num_heads;
@@ -99,19 +100,24 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   const uint32_t t_off = tr_lane_off<D>(lane);
 
   // Q/dO tiles and the tile's LSE (log2 units) and D values go straight to
-  // LDS.  Q and dO rows past the segment read as zero, so they add exactly
-  // nothing to dK/dV (their P and dS stay finite: S = 0, dP = 0); their LSE
-  // and D entries repeat the last row.  The loop issues no register loads,
-  // so the compiler places no waits on the in-flight tile loads.
+  // LDS.  Rows past the segment read as zero (the buffer range check), so
+  // they add exactly nothing to dK/dV: S = 0 and dP = 0 give finite P and
+  // dS = 0, and the zero dO row makes P's contribution to dV vanish.  The
+  // loop issues no register loads, so the compiler places no waits on the
+  // in-flight tile loads.
   const float* l2g = p.lse2 + (int64_t)it.q_start * H + it.head;
+  using Dma = TileDma<D, BQ>;
+  const uint32_t row_bytes = (uint32_t)rs * 2u, stat_bytes = (uint32_t)H * 4u;
+  Dma dma;
+  dma.init(wave, lane, row_bytes);
   auto fetch = [&](int q0, char* qdst, char* odst, float* ldst, float* ddst) {
-    const int nq = it.q_len - q0;  // >= 1: q0 is clamped into the segment
-    dma_tile<D, BQ, true>(qdst, qg + q0 * rs, rs, nq, wave, lane);
-    dma_tile<D, BQ, true>(odst, dog + q0 * rs, rs, nq, wave, lane);
+    const int nq = it.q_len - q0;
+    dma.issue(qdst, qg + (int64_t)q0 * rs, nq, row_bytes);
+    dma.issue(odst, dog + (int64_t)q0 * rs, nq, row_bytes);
     if (wave < 2) {
-      const int rc = min(q0 + lane, it.q_len - 1);
-      dma4((wave == 0 ? l2g : dsg) + (int64_t)rc * H,
-           __builtin_amdgcn_readfirstlane(lds_addr(wave == 0 ? ldst : ddst)));
+      const int nv = min(nq, BQ);
+      const i32x4 rsrc = buf_rsrc((wave == 0 ? l2g : dsg) + (int64_t)q0 * H, nv > 0 ? (nv - 1) * stat_bytes + 4u : 0u);
+      dma4(rsrc, lane * stat_bytes, __builtin_amdgcn_readfirstlane(lds_addr(wave == 0 ? ldst : ddst)));
     }
   };
 
@@ -199,19 +205,19 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
 
   // Ping-pong over the two buffer sets, unrolled by two so each half names
   // its buffers statically.  The next tile is fetched unconditionally (past
-  // the segment it reloads the last row, never read as data): the loop body
-  // stays free of branches, which keeps the dK/dV accumulators in place.
+  // the segment it reads zero and is never used): the loop body stays free
+  // of branches, which keeps the dK/dV accumulators in place.
   fetch(0, qs0, dos0, lse0, dsm0);
   wait_vmem();
   for (int q0 = 0;;) {
     __syncthreads();  // buffers 0 complete; buffers 1 no longer read
-    fetch(min(q0 + BQ, it.q_len - 1), qs1, dos1, lse1, dsm1);
+    fetch(q0 + BQ, qs1, dos1, lse1, dsm1);
     step(qs0, dos0, lse0, dsm0);
     wait_vmem();
     q0 += BQ;
     if (q0 >= it.q_len) break;
     __syncthreads();  // buffers 1 complete; buffers 0 no longer read
-    fetch(min(q0 + BQ, it.q_len - 1), qs0, dos0, lse0, dsm0);
+    fetch(q0 + BQ, qs0, dos0, lse0, dsm0);
     step(qs1, dos1, lse1, dsm1);
     wait_vmem();
     q0 += BQ;
@@ -247,7 +253,8 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
   // Two buffers of each tile as separate objects (see the dK/dV kernel).
   __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], vs0[TILE], vs1[TILE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ln = lane & 31, g = lane >> 5;
   const Item it = p.q_items[dispatch_item(blockIdx.x, p.n_q_items, p.xcd_chunk)];
   const int H = p.num_heads;
@@ -287,12 +294,17 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
     *ro = r;
     *kto = kt;
   };
+  // Rows past a range's end read zero; the step masks those keys.
+  using Dma = TileDma<D, BN>;
+  const uint32_t row_bytes = (uint32_t)rs * 2u;
+  Dma dma;
+  dma.init(wave, lane, row_bytes);
   auto fetch = [&](int r, int kt, char* kdst, char* vdst) {
     const int k0 = p.cu_k[r] + kt, nvalid = p.cu_k[r + 1] - k0;
     const uint16_t* kb_ = static_cast<const uint16_t*>(p.k) + ((int64_t)k0 * H + it.head) * D;
     const uint16_t* vb_ = static_cast<const uint16_t*>(p.v) + ((int64_t)k0 * H + it.head) * D;
-    dma_tile<D, BN>(kdst, kb_, rs, nvalid, wave, lane);
-    dma_tile<D, BN>(vdst, vb_, rs, nvalid, wave, lane);
+    dma.issue(kdst, kb_, nvalid, row_bytes);
+    dma.issue(vdst, vb_, nvalid, row_bytes);
   };
 
   auto step = [&](const char* kbuf, const char* vbuf, int nvalid) {

@@ -1,9 +1,9 @@
 // Packed whole+shard attention forward, bf16 inputs, gfx950 MFMA.
 //
-// One workgroup (4 waves) takes one work item: up to 128 query rows of one
-// head against one K/V range (a whole segment's own keys, or one CP block of
-// a shard, Sec. IV-D / Tab. II of arXiv 2608.01150).  Each wave owns 32 query
-// rows.  Per 64-key step:
+// One workgroup (8 waves, two per SIMD) takes one work item: up to 256 query
+// rows of one head against one K/V range (a whole segment's own keys, or one
+// CP block of a shard, Sec. IV-D / Tab. II of arXiv 2608.01150).  Each wave
+// owns 32 query rows.  Per 64-key step:
 //   S^T = K Q^T          MFMA 32x32x16 bf16, K from LDS (A), Q in registers (B)
 //   online softmax       per query in the lane's registers (exp2 domain)
 //   O^T += V^T P^T       MFMA, V^T from LDS by transpose reads (A), P^T
@@ -11,9 +11,10 @@
 // Computing the transposed products keeps one query per lane, so the row max
 // needs a single cross-lane exchange (lanes l and l^32) and the softmax
 // output is already the B operand of the next MFMA.  K and V tiles are staged
-// row-major (padded pitch, conflict-free) in double-buffered LDS by direct
-// global-to-LDS loads issued while the previous tile computes, one barrier
-// per step.
+// row-major (padded pitch, conflict-free) in three LDS buffers by direct
+// global-to-LDS loads issued two steps ahead (waves 0-3 load K, waves 4-7
+// load V), one barrier per step.  A staged tile serves 256 queries, so the
+// staging costs half as much per MFMA as with 128-row items.
 //
 // Epilogue: WHOLE items write the final bf16 output and the LSE; SHARD items
 // write the block-normalised fp32 partial and its LSE into their CP slot.
@@ -25,7 +26,7 @@ namespace zl {
 namespace {
 
 constexpr int BN = kFwdTileN;
-constexpr int NT = 256;
+constexpr int NT = 512;
 
 // Rescale the running output only when the running maximum grows by more
 // than 2^8 (log2 units): exp2 of scores against a stale maximum stays below
@@ -33,14 +34,18 @@ constexpr int NT = 256;
 constexpr float kRescaleSlack = 8.f;
 
 template <int D>
-__global__ __launch_bounds__(NT, 2) void fwd_bf16_kernel(FwdParams p) {
+__global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
   constexpr int PITCH = Pad<D>::PITCH;
   constexpr int TILE = BN * PITCH;
-  // Two buffers of each tile as separate objects, so the compiler can tell the
-  // direct-to-LDS loads filling one buffer from the reads of the other.
-  __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], vs0[TILE], vs1[TILE];
+  using Dma = TileDma<D, BN>;
+  // Per-wave direct-to-LDS instructions of one fetch (four waves share a tile).
+  constexpr int DMA_PER_FETCH = Dma::PER_WAVE;
+  // Three buffers of each tile as separate objects, so the compiler can tell
+  // the direct-to-LDS loads filling one buffer from the reads of another.
+  __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], ks2[TILE], vs0[TILE], vs1[TILE], vs2[TILE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ln = lane & 31, g = lane >> 5;
   const Item it = p.items[dispatch_item(blockIdx.x, p.n_items, p.xcd_chunk)];
   const int64_t rs = (int64_t)p.num_heads * D;  // elements between consecutive tokens
@@ -70,12 +75,16 @@ __global__ __launch_bounds__(NT, 2) void fwd_bf16_kernel(FwdParams p) {
   const uint32_t a_off = poff<D>(perm32(ln), g * 8);
   const uint32_t t_off = tr_lane_off<D>(lane);
 
-  // K/V tile starting at key kt (clamped into the range: rows past it reload
-  // the last key, masked below).
+  // K/V tile starting at key kt; rows past the range (and whole tiles past
+  // it, fetched by the lookahead) read zero and are masked below.  Waves 0-3
+  // load the K tile, waves 4-7 the V tile; the choice is wave-uniform.
+  const bool loads_k = wave < 4;
+  const uint16_t* src0 = loads_k ? kg : vg;
+  const uint32_t row_bytes = (uint32_t)rs * 2u;
+  Dma dma;
+  dma.init(wave & 3, lane, row_bytes);
   auto fetch = [&](int kt, char* kdst, char* vdst) {
-    const int nvalid = it.k_len - kt;
-    dma_tile<D, BN>(kdst, kg + kt * rs, rs, nvalid, wave, lane);
-    dma_tile<D, BN>(vdst, vg + kt * rs, rs, nvalid, wave, lane);
+    dma.issue(loads_k ? kdst : vdst, src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
   };
 
   auto step = [&](const char* kbuf, const char* vbuf, int kt) {
@@ -145,25 +154,36 @@ __global__ __launch_bounds__(NT, 2) void fwd_bf16_kernel(FwdParams p) {
     }
   };
 
-  // Ping-pong over the two buffer sets, unrolled by two; the next tile is
-  // fetched unconditionally (clamped into the range).
+  // Three buffer sets in rotation, the loop unrolled by three.  Tile t+2 is
+  // fetched right after the barrier that retires tile t-1's buffers, so every
+  // tile has two steps to arrive; fetches past the range read zero (an empty
+  // resource) and are never used.  Before the barrier a wave waits only for its own loads of
+  // tile t: the DMA_PER_FETCH loads of tile t+1 it issued later may stay in
+  // flight.
   if (it.k_len > 0) {
     fetch(0, ks0, vs0);
-    wait_vmem();
+    fetch(BN, ks1, vs1);
     for (int kt = 0;;) {
-      __syncthreads();  // buffers 0 complete; buffers 1 no longer read
-      fetch(min(kt + BN, it.k_len - 1), ks1, vs1);
+      wait_vmem_keep<DMA_PER_FETCH>();
+      __syncthreads();  // tile in buffers 0 complete; buffers 2 no longer read
+      fetch(kt + 2 * BN, ks2, vs2);
       step(ks0, vs0, kt);
-      wait_vmem();
       kt += BN;
       if (kt >= it.k_len) break;
-      __syncthreads();  // buffers 1 complete; buffers 0 no longer read
-      fetch(min(kt + BN, it.k_len - 1), ks0, vs0);
+      wait_vmem_keep<DMA_PER_FETCH>();
+      __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
+      fetch(kt + 2 * BN, ks0, vs0);
       step(ks1, vs1, kt);
-      wait_vmem();
+      kt += BN;
+      if (kt >= it.k_len) break;
+      wait_vmem_keep<DMA_PER_FETCH>();
+      __syncthreads();  // tile in buffers 2 complete; buffers 1 no longer read
+      fetch(kt + 2 * BN, ks1, vs1);
+      step(ks2, vs2, kt);
       kt += BN;
       if (kt >= it.k_len) break;
     }
+    wait_vmem();  // the lookahead loads must land before the workgroup's LDS is released
   }
 
   // Epilogue.  o[db][i] is (d = db*32 + 16*(i/8) + 8*g + i%8, query qr).

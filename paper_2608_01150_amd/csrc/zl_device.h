@@ -66,61 +66,92 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(size_t)((const __attribute__((address_space(3))) char*)p);
 }
 
-// One direct global->LDS 16-byte load per lane (global_load_lds_dwordx4): lane
-// l's 16 bytes land at the wave-uniform LDS address `lds` + 16*l.  Issued as
-// inline asm (M0 saved and restored around it) so that the compiler does not
-// treat it as an LDS store that every later LDS read must wait for; callers
-// wait for vmcnt themselves before the barrier that publishes the data.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer resource (stride 0, no swizzle) over `bytes` bytes at `base`.
+// A buffer load at a byte offset at or past `bytes` reads zero: the hardware
+// range check replaces per-lane clamping of addresses.
+__device__ __forceinline__ i32x4 buf_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  return i32x4{(int)(uint32_t)a, (int)((a >> 32) & 0xFFFFu), (int)bytes, 0x00020000};
+}
+
+// One direct buffer->LDS load per lane (buffer_load_dwordx4 ... lds): lane l's
+// 16 bytes, read at byte offset voff of the resource, land at the
+// wave-uniform LDS address `lds` + 16*l.  Issued as inline asm (M0 saved and
+// restored around it) so that the compiler does not treat it as an LDS store
+// that every later LDS read must wait for; callers wait for vmcnt themselves
+// before the barrier that publishes the data.  The s_nop is the one wait
+// state an LDS DMA needs after an SALU write of M0.
+__device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, uint32_t lds) {
   uint32_t save;
-  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds\n\ts_mov_b32 m0, %0"
                : "=&s"(save)
-               : "v"(g), "s"(lds)
+               : "v"(voff), "s"(rsrc), "s"(lds)
                : "memory");
 }
 
-// Same for 4 bytes per lane (global_load_lds_dword): lane l lands at lds + 4*l.
-__device__ __forceinline__ void dma4(const void* g, uint32_t lds) {
+// Same for 4 bytes per lane (buffer_load_dword ... lds): lane l lands at lds + 4*l.
+__device__ __forceinline__ void dma4(const i32x4& rsrc, uint32_t voff, uint32_t lds) {
   uint32_t save;
-  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds\n\ts_mov_b32 m0, %0"
                : "=&s"(save)
-               : "v"(g), "s"(lds)
+               : "v"(voff), "s"(rsrc), "s"(lds)
                : "memory");
 }
 
-// 16 zero bytes in device memory: the source of tile rows that must read as zero.
-static __device__ __attribute__((aligned(16))) const uint32_t kZeroChunk[4] = {0u, 0u, 0u, 0u};
-
-// Stage rows [0, ROWS) of one head of a packed [T, H, D] bf16 tensor (row 0
-// at g_row0, `rs` elements between rows) into a padded LDS tile with direct
-// global->LDS 16-byte loads (dma16).  A 64-row tile is a whole number of
-// 64-slot wave instructions (19 of them for D = 128, 9 for D = 64); each of
-// the 4 waves issues ceil(NJ/4) of them, the surplus ones clamped onto the
-// last block (rewriting identical bytes), so there is no branch.  Padding
-// slots reload chunk 0 of their row.  Rows at or past `nvalid` (>= 1) reload
-// row nvalid-1 (finite data the caller masks) or, with ZERO_TAIL, read as
-// zero.  Completion is tracked by vmcnt; callers wait before the barrier that
-// publishes the tile.
-template <int D, int ROWS, bool ZERO_TAIL = false>
-__device__ __forceinline__ void dma_tile(char* tile, const uint16_t* g_row0, int64_t rs, int nvalid, int wave,
-                                         int lane) {
-  constexpr int SPR = Pad<D>::PITCH / 16;
-  constexpr int NJ = ROWS * SPR / 64;
+// Staging of a [ROWS][D] bf16 tile of one head of a packed [T, H, D] tensor
+// (consecutive rows `row_bytes` apart in memory) into a padded LDS tile with
+// direct 16-byte loads.  The tile is NJ = ROWS * PITCH / 1024 whole wave
+// instructions; NW waves share them, each issuing PER_WAVE, the surplus ones
+// clamped onto the last block (rewriting identical bytes), so there is no
+// branch.  Padding slots reload chunk 0 of their row.  A lane's byte offsets
+// do not depend on the tile's position, so they are computed once; per tile
+// only the (scalar) buffer resource changes, and rows at or past the range
+// end read as zero through its range check.
+template <int D, int ROWS, int NW = 4>
+struct TileDma {
+  static constexpr int SPR = Pad<D>::PITCH / 16;
+  static constexpr int NJ = ROWS * SPR / 64;
+  static constexpr int PER_WAVE = (NJ + NW - 1) / NW;
   static_assert(ROWS * SPR % 64 == 0, "tile must be whole wave instructions");
+  uint32_t voff[PER_WAVE];
+  int wave;  // wave-uniform index in [0, NW)
+
+  __device__ __forceinline__ void init(int wave_, int lane, uint32_t row_bytes) {
+    wave = wave_;
 #pragma unroll
-  for (int jj = 0; jj < (NJ + 3) / 4; ++jj) {
-    const int j = min(wave + 4 * jj, NJ - 1);
-    const int slot = j * 64 + lane;
-    const int row = slot / SPR, chunk = slot % SPR;
-    const int rr = min(row, nvalid - 1);
-    const int cc = chunk < D / 8 ? chunk : 0;
-    const void* src = g_row0 + rr * rs + cc * 8;
-    if (ZERO_TAIL && row >= nvalid) src = kZeroChunk;
-    dma16(src, __builtin_amdgcn_readfirstlane(lds_addr(tile) + j * 1024));
+    for (int jj = 0; jj < PER_WAVE; ++jj) {
+      const int j = min(wave + NW * jj, NJ - 1);
+      const int slot = j * 64 + lane;
+      const int row = slot / SPR, chunk = slot % SPR;
+      voff[jj] = (uint32_t)row * row_bytes + (uint32_t)(chunk < D / 8 ? chunk : 0) * 16u;
+    }
   }
-}
+
+  // Rows [0, ROWS) starting at g_row0; rows at or past nvalid read zero.
+  __device__ __forceinline__ void issue(char* tile, const void* g_row0, int nvalid, uint32_t row_bytes) const {
+    const int nv = min(nvalid, ROWS);
+    const uint32_t bytes = nv > 0 ? (uint32_t)(nv - 1) * row_bytes + D * 2 : 0u;
+    const i32x4 rsrc = buf_rsrc(g_row0, bytes);
+#pragma unroll
+    for (int jj = 0; jj < PER_WAVE; ++jj) {
+      const int j = min(wave + NW * jj, NJ - 1);
+      dma16(rsrc, voff[jj], __builtin_amdgcn_readfirstlane(lds_addr(tile) + j * 1024));
+    }
+  }
+};
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Wait until at most N of this wave's vector memory loads are outstanding.
+// Loads complete in issue order, so this retires everything but the N most
+// recent (a tile fetched ahead of the one about to be used).
+template <int N>
+__device__ __forceinline__ void wait_vmem_keep() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 

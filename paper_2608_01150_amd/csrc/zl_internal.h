@@ -20,7 +20,7 @@ static_assert(sizeof(Item) == 32, "work item must stay 32 bytes");
 
 // Tile shapes of each kernel family (rows of Q per forward item, keys per
 // backward item, and the inner tile of the loop each one runs).
-constexpr int kFwdTileM = 128;       // bf16 forward: 4 waves x 32 query rows
+constexpr int kFwdTileM = 256;       // bf16 forward: 4 waves x 64 query rows
 constexpr int kFwdTileN = 64;        // keys per inner step
 constexpr int kFwd32TileM = 64;      // fp32 forward: one query row per lane
 constexpr int kFwd32TileN = 32;
