@@ -62,10 +62,9 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   constexpr int BQ = kBwdTileM;                 // 64 queries per step
   constexpr int PITCH = Pad<D>::PITCH;
   constexpr int TILE = BQ * PITCH;              // bytes of one Q (or dO) tile
-  // Two buffers of each tile as separate objects, so the compiler can tell the
-  // direct-to-LDS loads filling one buffer from the reads of the other.
-  __shared__ __attribute__((aligned(16))) char qs0[TILE], qs1[TILE], dos0[TILE], dos1[TILE];
-  __shared__ __attribute__((aligned(16))) float lse0[BQ], lse1[BQ], dsm0[BQ], dsm1[BQ];
+  // Two buffers of each tile (Q, dO) and of the tile's LSE and D values.
+  __shared__ __attribute__((aligned(16))) char qs[2][TILE], dos[2][TILE];
+  __shared__ __attribute__((aligned(16))) float lss[2][BQ], dss[2][BQ];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -95,6 +94,11 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
     dv[db] = f32x16{};
   }
   __builtin_amdgcn_s_waitcnt(0);  // prologue loads done (see the forward kernel)
+  // The K/V fragments are only ever MFMA B operands, which may come from
+  // AGPRs: keeping them there leaves the arch VGPRs to S, dP and the LDS
+  // operands, so the MFMA results feeding the softmax need no copies.
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) asm volatile("" : "+a"(kf[kk]), "+a"(vf[kk]));
 
   const uint32_t a_off = poff<D>(perm32(ln), g * 8);
   const uint32_t t_off = tr_lane_off<D>(lane);
@@ -114,11 +118,12 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
     const int nq = it.q_len - q0;
     dma.issue(qdst, qg + (int64_t)q0 * rs, nq, row_bytes);
     dma.issue(odst, dog + (int64_t)q0 * rs, nq, row_bytes);
-    if (wave < 2) {
-      const int nv = min(nq, BQ);
-      const i32x4 rsrc = buf_rsrc((wave == 0 ? l2g : dsg) + (int64_t)q0 * H, nv > 0 ? (nv - 1) * stat_bytes + 4u : 0u);
-      dma4(rsrc, lane * stat_bytes, __builtin_amdgcn_readfirstlane(lds_addr(wave == 0 ? ldst : ddst)));
-    }
+    // Even waves load the LSE row, odd waves D (waves 2 and 3 repeat 0 and 1,
+    // rewriting identical bytes): no branch in the loop body.
+    const bool even = (wave & 1) == 0;
+    const int nv = min(nq, BQ);
+    const i32x4 rsrc = buf_rsrc((even ? l2g : dsg) + (int64_t)q0 * H, nv > 0 ? (nv - 1) * stat_bytes + 4u : 0u);
+    dma4(rsrc, lane * stat_bytes, __builtin_amdgcn_readfirstlane(lds_addr(even ? ldst : ddst)));
   };
 
   // One 64-query step on the tiles (qt_, ot_, ls, ds).
@@ -203,22 +208,22 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
     dvdk(1, pp1, pds1);
   };
 
-  // Ping-pong over the two buffer sets, unrolled by two so each half names
-  // its buffers statically.  The next tile is fetched unconditionally (past
-  // the segment it reads zero and is never used): the loop body stays free
-  // of branches, which keeps the dK/dV accumulators in place.
-  fetch(0, qs0, dos0, lse0, dsm0);
+  // Ping-pong over the two buffer sets in a rolled loop (the buffer is an
+  // index: the asm DMA is opaque to the compiler, so naming the buffers
+  // statically buys nothing, and one loop body keeps the dK/dV accumulators in
+  // the same registers on every iteration).  The next tile is fetched
+  // unconditionally (past the segment it reads zero and is never used): the
+  // loop body stays free of branches.
+  fetch(0, qs[0], dos[0], lss[0], dss[0]);
   wait_vmem();
-  for (int q0 = 0;;) {
-    __syncthreads();  // buffers 0 complete; buffers 1 no longer read
-    fetch(q0 + BQ, qs1, dos1, lse1, dsm1);
-    step(qs0, dos0, lse0, dsm0);
-    wait_vmem();
-    q0 += BQ;
-    if (q0 >= it.q_len) break;
-    __syncthreads();  // buffers 1 complete; buffers 0 no longer read
-    fetch(q0 + BQ, qs0, dos0, lse0, dsm0);
-    step(qs1, dos1, lse1, dsm1);
+  for (int q0 = 0, b = 0;; b ^= 1) {
+    __syncthreads();  // buffers b complete; buffers b^1 no longer read
+    fetch(q0 + BQ, qs[b ^ 1], dos[b ^ 1], lss[b ^ 1], dss[b ^ 1]);
+    step(qs[b], dos[b], lss[b], dss[b]);
+    // The accumulators are only MFMA C/D operands: keep them in AGPRs across
+    // the back edge, so the register allocator does not move them.
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) asm volatile("" : "+a"(dk[db]), "+a"(dv[db]));
     wait_vmem();
     q0 += BQ;
     if (q0 >= it.q_len) break;
