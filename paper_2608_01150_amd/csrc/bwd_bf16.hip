@@ -126,86 +126,114 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
     dma4(rsrc, lane * stat_bytes, __builtin_amdgcn_readfirstlane(lds_addr(even ? ldst : ddst)));
   };
 
-  // One 64-query step on the tiles (qt_, ot_, ls, ds).
+  // One 64-query step on the tiles, as two 32-query sub-blocks sb and four
+  // phases of D/8 MFMAs each:
+  //   A(sb)  S = Q K^T and dP = dO V^T            (Q, dO rows from LDS)
+  //   B(sb)  P = exp(S - LSE), dS = P (dP - D)    (VALU, packed to bf16)
+  //   C(sb)  dV^T += dO^T P, dK^T += Q^T dS       (dO^T, Q^T by transpose reads)
+  // issued as A(0) | A(1)+B(0) | C(0)+B(1) | C(1): the softmax of one
+  // sub-block is cut into 8 chunks that alternate with the other's MFMAs, so
+  // the matrix cores and the VALU work at the same time.  Every MFMA's LDS
+  // operand is read a few MFMAs ahead through a small register ring.  The
+  // order is fixed with scheduling fences: the compiler's own schedule
+  // clusters the MFMAs and the VALU work and waits on each operand read.
+  constexpr int NM = D / 8;   // MFMAs per phase
+  constexpr int PFA = 4;      // operand lookahead, A phases (one b128 read each)
+  constexpr int PFC = 3;      // operand lookahead, C phases (two transpose reads each)
   auto step = [&](const char* qbuf, const char* obuf, const float* ls, const float* ds) {
     const char* qa = qbuf + a_off;
     const char* oa = obuf + a_off;
     const char* qt = qbuf + t_off;
     const char* ot = obuf + t_off;
-    // S and dP of sub-block sb (32 queries): D row m <-> query sb*32 +
-    // perm32(m); register i <-> query sb*32 + 16*(i/8) + 8g + i%8.
-    auto sdp = [&](int sb, f32x16& s, f32x16& dp) {
-      s = f32x16{};
-      dp = f32x16{};
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        s = mfma32(*reinterpret_cast<const u32x4*>(qa + poff<D>(sb * 32, kk * 16)), kf[kk], s);
-        dp = mfma32(*reinterpret_cast<const u32x4*>(oa + poff<D>(sb * 32, kk * 16)), vf[kk], dp);
-      }
-    };
-    // P = exp(S - LSE), dS = P (dP - D), packed as bf16 B operands (k = queries).
-    auto softmax = [&](int sb, const f32x16& s, const f32x16& dp, u32x4* pp, u32x4* pds) {
+    // S, dP of sub-block sb: D row m <-> query sb*32 + perm32(m); register i
+    // <-> query sb*32 + 16*(i/8) + 8g + i%8 (lane = key).
+    f32x16 s[2], dp[2];
+    u32x4 pp[2][2], pds[2][2];  // [sb][h]: bf16 B operands, k = queries 16h + 8g ..
+    f32x4 lsv[2][2][2], dsv[2][2][2];  // [sb][h][half]: LSE (log2) and D of those queries
+
+    auto load_stats = [&](int sb) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int q8 = sb * 32 + 16 * h + 8 * g;
-        const f32x4 l0 = *reinterpret_cast<const f32x4*>(&ls[q8]);
-        const f32x4 l1 = *reinterpret_cast<const f32x4*>(&ls[q8 + 4]);
-        const f32x4 d0 = *reinterpret_cast<const f32x4*>(&ds[q8]);
-        const f32x4 d1 = *reinterpret_cast<const f32x4*>(&ds[q8 + 4]);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          float pv[2], dsv[2];
-#pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            const int tt = 2 * t + e, i = 8 * h + tt;
-            const float l2 = tt < 4 ? l0[tt] : l1[tt - 4];
-            const float dd = tt < 4 ? d0[tt] : d1[tt - 4];
-            // A key past the range (k_ok false) only feeds its own dK/dV, never stored.
-            const float pr = fast_exp2(fmaf(s[i], p.scale_log2, -l2));
-            pv[e] = pr;
-            dsv[e] = pr * (dp[i] - dd);
-          }
-          pp[h][t] = pack_bf16(pv[0], pv[1]);
-          pds[h][t] = pack_bf16(dsv[0], dsv[1]);
+        for (int e = 0; e < 2; ++e) {
+          lsv[sb][h][e] = *reinterpret_cast<const f32x4*>(&ls[q8 + 4 * e]);
+          dsv[sb][h][e] = *reinterpret_cast<const f32x4*>(&ds[q8 + 4 * e]);
         }
       }
     };
-    // dV^T += dO^T P and dK^T += Q^T dS; A row m <-> d = db*32 + perm32(m), k <-> queries.
-    auto dvdk = [&](int sb, const u32x4* pp, const u32x4* pds) {
+    // Chunk c (0..7) of B(sb): elements 2c, 2c+1 -> one packed word of P and of dS.
+    // A key past the range (k_ok false) only feeds its own dK/dV, never stored.
+    auto chunk = [&](int sb, int c) {
+      const int h = c >> 2, t = c & 3;
+      float pv[2], dv_[2];
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
+      for (int e = 0; e < 2; ++e) {
+        const int tt = 2 * t + e, i = 8 * h + tt;
+        const float l2 = lsv[sb][h][tt >> 2][tt & 3];
+        const float dd = dsv[sb][h][tt >> 2][tt & 3];
+        pv[e] = fast_exp2(fmaf(s[sb][i], p.scale_log2, -l2));
+        dv_[e] = pv[e] * (dp[sb][i] - dd);
+      }
+      pp[sb][h][t] = pack_bf16(pv[0], pv[1]);
+      pds[sb][h][t] = pack_bf16(dv_[0], dv_[1]);
+    };
+    // Chunk k of the partner softmax goes after MFMA j = k*NM/8 + NM/8 - 1.
+    auto chunk_at = [&](int other, int j) {
+      if (other >= 0 && (j % (NM / 8)) == NM / 8 - 1) chunk(other, j / (NM / 8));
+    };
+
+    // A(sb): operand j is the Q (even j) or dO (odd j) chunk k = j/2.
+    auto a_op = [&](int sb, int j) {
+      return *reinterpret_cast<const u32x4*>(((j & 1) ? oa : qa) + poff<D>(sb * 32, (j >> 1) * 16));
+    };
+    auto phaseA = [&](int sb, int other) {
+      s[sb] = f32x16{};
+      dp[sb] = f32x16{};
+      u32x4 ring[PFA];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          dv[db] = mfma32(tr_operand<D>(ot, sb * 32 + 16 * h, db * 32), pp[h], dv[db]);
-          dk[db] = mfma32(tr_operand<D>(qt, sb * 32 + 16 * h, db * 32), pds[h], dk[db]);
-        }
+      for (int j = 0; j < PFA; ++j) ring[j] = a_op(sb, j);
+      load_stats(sb);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < NM; ++j) {
+        const u32x4 a = ring[j % PFA];
+        if (j + PFA < NM) ring[j % PFA] = a_op(sb, j + PFA);
+        if (j & 1)
+          dp[sb] = mfma32(a, vf[j >> 1], dp[sb]);
+        else
+          s[sb] = mfma32(a, kf[j >> 1], s[sb]);
+        chunk_at(other, j);
+        __builtin_amdgcn_sched_barrier(0);
       }
     };
-    // Two-stage pipeline over the two sub-blocks: the MFMAs of one stage are
-    // interleaved with the softmax VALU work of the other.
-    f32x16 s0, dp0, s1, dp1;
-    u32x4 pp0[2], pds0[2], pp1[2], pds1[2];
-    sdp(0, s0, dp0);
-    __builtin_amdgcn_sched_barrier(0);
-    sdp(1, s1, dp1);
-    softmax(0, s0, dp0, pp0, pds0);
+    // C(sb): operand j -> h = j / (NM/2), db = (j % (NM/2)) / 2; even j dO^T (dV), odd j Q^T (dK).
+    auto c_op = [&](int sb, int j) {
+      const int h = j / (NM / 2), db = (j % (NM / 2)) >> 1;
+      return tr_operand<D>((j & 1) ? qt : ot, sb * 32 + 16 * h, db * 32);
+    };
+    auto phaseC = [&](int sb, int other) {
+      u32x4 ring[PFC];
 #pragma unroll
-    for (int i = 0; i < D / 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // five VALU
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    dvdk(0, pp0, pds0);
-    softmax(1, s1, dp1, pp1, pds1);
+      for (int j = 0; j < PFC; ++j) ring[j] = c_op(sb, j);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int i = 0; i < D / 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);  // one MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);  // two LDS reads (one transposed operand)
-      __builtin_amdgcn_sched_group_barrier(0x002, 5, 1);  // five VALU
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    dvdk(1, pp1, pds1);
+      for (int j = 0; j < NM; ++j) {
+        const u32x4 a = ring[j % PFC];
+        if (j + PFC < NM) ring[j % PFC] = c_op(sb, j + PFC);
+        const int h = j / (NM / 2), db = (j % (NM / 2)) >> 1;
+        if (j & 1)
+          dk[db] = mfma32(a, pds[sb][h], dk[db]);
+        else
+          dv[db] = mfma32(a, pp[sb][h], dv[db]);
+        chunk_at(other, j);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    phaseA(0, -1);
+    phaseA(1, 0);
+    phaseC(0, 1);
+    phaseC(1, -1);
   };
 
   // Ping-pong over the two buffer sets in a rolled loop (the buffer is an
