@@ -206,6 +206,9 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
         chunk_at(other, j);
         __builtin_amdgcn_sched_barrier(0);
       }
+      // S and dP are read by the VALU: move them to arch VGPRs once, here,
+      // so they never share AGPRs with the accumulators.
+      asm volatile("" : "+v"(s[sb]), "+v"(dp[sb]));
     };
     // C(sb): operand j -> h = j / (NM/2), db = (j % (NM/2)) / 2; even j dO^T (dV), odd j Q^T (dK).
     auto c_op = [&](int sb, int j) {
