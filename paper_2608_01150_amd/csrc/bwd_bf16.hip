@@ -57,208 +57,222 @@ __global__ __launch_bounds__(NT) void bwd_pre_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------------ dK / dV
+// Warp-specialised: a workgroup of 8 waves takes 128 keys.  Producer wave w
+// (0-3) and consumer wave w+4 share keys 32w .. 32w+31 and run on the same
+// SIMD.  Per 64-query step, as two 32-query sub-blocks sb:
+//   producer  S = Q K^T, dP = dO V^T (MFMA, K and V in registers), then
+//             P = exp(S - LSE), dS = P (dP - D) (VALU), written to LDS as the
+//             consumer's bf16 B operands;
+//   consumer  dV^T += dO^T P, dK^T += Q^T dS (MFMA, dO^T and Q^T by
+//             transpose reads of the staged tiles).
+// Two waves per SIMD with complementary work let the hardware overlap the
+// producer's softmax with the consumer's MFMAs; each role fits in half the
+// register file.  Phases, separated by workgroup barriers:
+//   phase 1 of step t: producer A+B of (t, sb 0) | consumer C of (t-1, sb 1)
+//   phase 2 of step t: producer A+B of (t, sb 1) | consumer C of (t, sb 0)
+// Q/dO tiles rotate through three buffers: tile t+2 is fetched after the
+// barrier ending phase 1 of step t (its buffer held tile t-1, whose last
+// reader was that phase) and must land before phase 1 of step t+2.
+constexpr int kDkdvThreads = 512;
+
 template <int D>
-__global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
+__global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) {
   constexpr int BQ = kBwdTileM;                 // 64 queries per step
   constexpr int PITCH = Pad<D>::PITCH;
   constexpr int TILE = BQ * PITCH;              // bytes of one Q (or dO) tile
-  // Two buffers of each tile (Q, dO) and of the tile's LSE and D values.
-  __shared__ __attribute__((aligned(16))) char qs[2][TILE], dos[2][TILE];
-  __shared__ __attribute__((aligned(16))) float lss[2][BQ], dss[2][BQ];
+  constexpr int NBUF = 3;
+  constexpr int NM = D / 8;                     // MFMAs per phase and role
+  __shared__ __attribute__((aligned(16))) char qs[NBUF][TILE], dos[NBUF][TILE];
+  __shared__ __attribute__((aligned(16))) float lss[NBUF][BQ], dss[NBUF][BQ];
+  // P/dS exchange: [sb][key group][word: P h0, P h1, dS h0, dS h1][lane].
+  __shared__ __attribute__((aligned(16))) u32x4 xch[2][4][4][64];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool producer = wave < 4;
+  const int kw = wave & 3;                      // key group
   const int ln = lane & 31, g = lane >> 5;
   const Item it = p.kv_items[dispatch_item(blockIdx.x, p.n_kv_items, p.xcd_chunk)];
   const int H = p.num_heads;
   const int64_t rs = (int64_t)H * D;
   const uint16_t* qg = static_cast<const uint16_t*>(p.q) + ((int64_t)it.q_start * H + it.head) * D;
   const uint16_t* dog = static_cast<const uint16_t*>(p.dout) + ((int64_t)it.q_start * H + it.head) * D;
-  const uint16_t* kg = static_cast<const uint16_t*>(p.k) + ((int64_t)it.k_start * H + it.head) * D;
-  const uint16_t* vg = static_cast<const uint16_t*>(p.v) + ((int64_t)it.k_start * H + it.head) * D;
+  const float* l2g = p.lse2 + (int64_t)it.q_start * H + it.head;
   const float* dsg = p.dsum + (int64_t)it.q_start * H + it.head;
-
-  // This lane's key (B-operand column) and its K, V fragments.
-  const int key = wave * 32 + ln;
+  const int key = kw * 32 + ln;
   const bool k_ok = key < it.k_len;
-  u32x4 kf[D / 16], vf[D / 16];
+  const int nsteps = (it.q_len + BQ - 1) / BQ;
+
+  const uint32_t a_off = poff<D>(perm32(ln), g * 8);
+  const uint32_t t_off = tr_lane_off<D>(lane);
+
+  // Staging: producers load the Q tile and the tile's LSE (log2 units, even
+  // waves) or D (odd waves; waves 2, 3 repeat 0, 1 with identical bytes);
+  // consumers load the dO tile.  Rows past the segment read as zero (the
+  // buffer range check), which adds exactly nothing to dK/dV: S = 0, dP = 0
+  // and D = 0 give finite P and dS = 0, and the zero dO row cancels P in dV.
+  using Dma = TileDma<D, BQ>;
+  constexpr int PER_FETCH_P = Dma::PER_WAVE + 1, PER_FETCH_C = Dma::PER_WAVE;
+  const uint32_t row_bytes = (uint32_t)rs * 2u, stat_bytes = (uint32_t)H * 4u;
+  Dma dma;
+  dma.init(kw, lane, row_bytes);
+  auto fetch = [&](int t) {
+    const int q0 = t * BQ, nq = it.q_len - q0, b = t % NBUF;
+    if (producer) {
+      dma.issue(qs[b], qg + (int64_t)q0 * rs, nq, row_bytes);
+      const bool even = (kw & 1) == 0;
+      const int nv = min(nq, BQ);
+      const i32x4 rsrc = buf_rsrc((even ? l2g : dsg) + (int64_t)q0 * H, nv > 0 ? (nv - 1) * stat_bytes + 4u : 0u);
+      dma4(rsrc, lane * stat_bytes, __builtin_amdgcn_readfirstlane(lds_addr(even ? lss[b] : dss[b])));
+    } else {
+      dma.issue(dos[b], dog + (int64_t)q0 * rs, nq, row_bytes);
+    }
+  };
+
+  fetch(0);
+  fetch(1);
+
+  if (producer) {
+    // ---------------------------------------------------------- producer
+    const uint16_t* kg = static_cast<const uint16_t*>(p.k) + ((int64_t)it.k_start * H + it.head) * D;
+    const uint16_t* vg = static_cast<const uint16_t*>(p.v) + ((int64_t)it.k_start * H + it.head) * D;
+    u32x4 kf[D / 16], vf[D / 16];
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
-    kf[kk] = k_ok ? *reinterpret_cast<const u32x4*>(kg + key * rs + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
-    vf[kk] = k_ok ? *reinterpret_cast<const u32x4*>(vg + key * rs + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
+    for (int kk = 0; kk < D / 16; ++kk) {
+      kf[kk] = k_ok ? *reinterpret_cast<const u32x4*>(kg + key * rs + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
+      vf[kk] = k_ok ? *reinterpret_cast<const u32x4*>(vg + key * rs + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
+    }
+    // Retire the fragment loads (and with them the two tile fetches issued
+    // before) with a waitcnt the compiler sees, so the loop carries no
+    // pending register loads and gets no vmcnt wait of the compiler's.
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();  // tile 0 published
+
+    constexpr int PFA = 4;
+    for (int t = 0; t < nsteps; ++t) {
+      const int b = t % NBUF;
+      const char* qa = qs[b] + a_off;
+      const char* oa = dos[b] + a_off;
+      const float* ls = lss[b];
+      const float* ds = dss[b];
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb) {
+        // A: S and dP of the sub-block; register i <-> query sb*32 + 16*(i/8) + 8g + i%8.
+        auto a_op = [&](int j) {
+          return *reinterpret_cast<const u32x4*>(((j & 1) ? oa : qa) + poff<D>(sb * 32, (j >> 1) * 16));
+        };
+        f32x16 sc = f32x16{}, dp = f32x16{};
+        u32x4 ring[PFA];
+#pragma unroll
+        for (int j = 0; j < PFA; ++j) ring[j] = a_op(j);
+        f32x4 lsv[2][2], dsv[2][2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const int q4 = sb * 32 + 16 * h + 8 * g + 4 * e;
+            lsv[h][e] = *reinterpret_cast<const f32x4*>(&ls[q4]);
+            dsv[h][e] = *reinterpret_cast<const f32x4*>(&ds[q4]);
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < NM; ++j) {
+          const u32x4 a = ring[j % PFA];
+          if (j + PFA < NM) ring[j % PFA] = a_op(j + PFA);
+          if (j & 1)
+            dp = mfma32(a, vf[j >> 1], dp);
+          else
+            sc = mfma32(a, kf[j >> 1], sc);
+        }
+        // B: P = exp(S - LSE), dS = P (dP - D), packed bf16 (k = queries 16h + 8g ..).
+        // A key past the range (k_ok false) only feeds its own dK/dV, never stored.
+        u32x4 pp[2], pds[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+#pragma unroll
+          for (int t2 = 0; t2 < 4; ++t2) {
+            float pv[2], dv_[2];
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+              const int tt = 2 * t2 + e, i = 8 * h + tt;
+              const float l2 = lsv[h][tt >> 2][tt & 3];
+              const float dd = dsv[h][tt >> 2][tt & 3];
+              pv[e] = fast_exp2(fmaf(sc[i], p.scale_log2, -l2));
+              dv_[e] = pv[e] * (dp[i] - dd);
+            }
+            pp[h][t2] = pack_bf16(pv[0], pv[1]);
+            pds[h][t2] = pack_bf16(dv_[0], dv_[1]);
+          }
+        }
+        xch[sb][kw][0][lane] = pp[0];
+        xch[sb][kw][1][lane] = pp[1];
+        xch[sb][kw][2][lane] = pds[0];
+        xch[sb][kw][3][lane] = pds[1];
+        if (sb == 0) {
+          __syncthreads();  // end of phase 1: P/dS of sub-block 0 published
+          fetch(t + 2);     // into the buffer of tile t-1, whose last reader was phase 1
+        } else {
+          wait_vmem_keep<PER_FETCH_P>();  // own loads of tile t+1 landed
+          __syncthreads();  // end of phase 2: P/dS of sub-block 1 and tile t+1 published
+        }
+      }
+    }
+    wait_vmem();  // the lookahead loads must land before the workgroup's LDS is released
+    return;
   }
+
+  // ------------------------------------------------------------ consumer
   f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) {
     dk[db] = f32x16{};
     dv[db] = f32x16{};
   }
-  __builtin_amdgcn_s_waitcnt(0);  // prologue loads done (see the forward kernel)
-  // The K/V fragments are only ever MFMA B operands, which may come from
-  // AGPRs: keeping them there leaves the arch VGPRs to S, dP and the LDS
-  // operands, so the MFMA results feeding the softmax need no copies.
-#pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) asm volatile("" : "+a"(kf[kk]), "+a"(vf[kk]));
+  wait_vmem_keep<PER_FETCH_C>();  // tile 0 landed (own loads)
+  __syncthreads();                // tile 0 published
 
-  const uint32_t a_off = poff<D>(perm32(ln), g * 8);
-  const uint32_t t_off = tr_lane_off<D>(lane);
-
-  // Q/dO tiles and the tile's LSE (log2 units) and D values go straight to
-  // LDS.  Rows past the segment read as zero (the buffer range check), so
-  // they add exactly nothing to dK/dV: S = 0 and dP = 0 give finite P and
-  // dS = 0, and the zero dO row makes P's contribution to dV vanish.  The
-  // loop issues no register loads, so the compiler places no waits on the
-  // in-flight tile loads.
-  const float* l2g = p.lse2 + (int64_t)it.q_start * H + it.head;
-  using Dma = TileDma<D, BQ>;
-  const uint32_t row_bytes = (uint32_t)rs * 2u, stat_bytes = (uint32_t)H * 4u;
-  Dma dma;
-  dma.init(wave, lane, row_bytes);
-  auto fetch = [&](int q0, char* qdst, char* odst, float* ldst, float* ddst) {
-    const int nq = it.q_len - q0;
-    dma.issue(qdst, qg + (int64_t)q0 * rs, nq, row_bytes);
-    dma.issue(odst, dog + (int64_t)q0 * rs, nq, row_bytes);
-    // Even waves load the LSE row, odd waves D (waves 2 and 3 repeat 0 and 1,
-    // rewriting identical bytes): no branch in the loop body.
-    const bool even = (wave & 1) == 0;
-    const int nv = min(nq, BQ);
-    const i32x4 rsrc = buf_rsrc((even ? l2g : dsg) + (int64_t)q0 * H, nv > 0 ? (nv - 1) * stat_bytes + 4u : 0u);
-    dma4(rsrc, lane * stat_bytes, __builtin_amdgcn_readfirstlane(lds_addr(even ? ldst : ddst)));
-  };
-
-  // One 64-query step on the tiles, as two 32-query sub-blocks sb and four
-  // phases of D/8 MFMAs each:
-  //   A(sb)  S = Q K^T and dP = dO V^T            (Q, dO rows from LDS)
-  //   B(sb)  P = exp(S - LSE), dS = P (dP - D)    (VALU, packed to bf16)
-  //   C(sb)  dV^T += dO^T P, dK^T += Q^T dS       (dO^T, Q^T by transpose reads)
-  // issued as A(0) | A(1)+B(0) | C(0)+B(1) | C(1): the softmax of one
-  // sub-block is cut into 8 chunks that alternate with the other's MFMAs, so
-  // the matrix cores and the VALU work at the same time.  Every MFMA's LDS
-  // operand is read a few MFMAs ahead through a small register ring.  The
-  // order is fixed with scheduling fences: the compiler's own schedule
-  // clusters the MFMAs and the VALU work and waits on each operand read.
-  constexpr int NM = D / 8;   // MFMAs per phase
-  constexpr int PFA = 4;      // operand lookahead, A phases (one b128 read each)
-  constexpr int PFC = 3;      // operand lookahead, C phases (two transpose reads each)
-  auto step = [&](const char* qbuf, const char* obuf, const float* ls, const float* ds) {
-    const char* qa = qbuf + a_off;
-    const char* oa = obuf + a_off;
-    const char* qt = qbuf + t_off;
-    const char* ot = obuf + t_off;
-    // S, dP of sub-block sb: D row m <-> query sb*32 + perm32(m); register i
-    // <-> query sb*32 + 16*(i/8) + 8g + i%8 (lane = key).
-    f32x16 s[2], dp[2];
-    u32x4 pp[2][2], pds[2][2];  // [sb][h]: bf16 B operands, k = queries 16h + 8g ..
-    f32x4 lsv[2][2][2], dsv[2][2][2];  // [sb][h][half]: LSE (log2) and D of those queries
-
-    auto load_stats = [&](int sb) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int q8 = sb * 32 + 16 * h + 8 * g;
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          lsv[sb][h][e] = *reinterpret_cast<const f32x4*>(&ls[q8 + 4 * e]);
-          dsv[sb][h][e] = *reinterpret_cast<const f32x4*>(&ds[q8 + 4 * e]);
-        }
-      }
-    };
-    // Chunk c (0..7) of B(sb): elements 2c, 2c+1 -> one packed word of P and of dS.
-    // A key past the range (k_ok false) only feeds its own dK/dV, never stored.
-    auto chunk = [&](int sb, int c) {
-      const int h = c >> 2, t = c & 3;
-      float pv[2], dv_[2];
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int tt = 2 * t + e, i = 8 * h + tt;
-        const float l2 = lsv[sb][h][tt >> 2][tt & 3];
-        const float dd = dsv[sb][h][tt >> 2][tt & 3];
-        pv[e] = fast_exp2(fmaf(s[sb][i], p.scale_log2, -l2));
-        dv_[e] = pv[e] * (dp[sb][i] - dd);
-      }
-      pp[sb][h][t] = pack_bf16(pv[0], pv[1]);
-      pds[sb][h][t] = pack_bf16(dv_[0], dv_[1]);
-    };
-    // Chunk k of the partner softmax goes after MFMA j = k*NM/8 + NM/8 - 1.
-    auto chunk_at = [&](int other, int j) {
-      if (other >= 0 && (j % (NM / 8)) == NM / 8 - 1) chunk(other, j / (NM / 8));
-    };
-
-    // A(sb): operand j is the Q (even j) or dO (odd j) chunk k = j/2.
-    auto a_op = [&](int sb, int j) {
-      return *reinterpret_cast<const u32x4*>(((j & 1) ? oa : qa) + poff<D>(sb * 32, (j >> 1) * 16));
-    };
-    auto phaseA = [&](int sb, int other) {
-      s[sb] = f32x16{};
-      dp[sb] = f32x16{};
-      u32x4 ring[PFA];
-#pragma unroll
-      for (int j = 0; j < PFA; ++j) ring[j] = a_op(sb, j);
-      load_stats(sb);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int j = 0; j < NM; ++j) {
-        const u32x4 a = ring[j % PFA];
-        if (j + PFA < NM) ring[j % PFA] = a_op(sb, j + PFA);
-        if (j & 1)
-          dp[sb] = mfma32(a, vf[j >> 1], dp[sb]);
-        else
-          s[sb] = mfma32(a, kf[j >> 1], s[sb]);
-        chunk_at(other, j);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      // S and dP are read by the VALU: move them to arch VGPRs once, here,
-      // so they never share AGPRs with the accumulators.
-      asm volatile("" : "+v"(s[sb]), "+v"(dp[sb]));
-    };
-    // C(sb): operand j -> h = j / (NM/2), db = (j % (NM/2)) / 2; even j dO^T (dV), odd j Q^T (dK).
-    auto c_op = [&](int sb, int j) {
+  constexpr int PFC = 3;
+  // C(sb) of tile t: operand j -> h = j / (NM/2), db = (j % (NM/2)) / 2; even j
+  // dO^T (dV), odd j Q^T (dK); A row m <-> d = db*32 + perm32(m), k <-> queries.
+  auto phaseC = [&](int t, int sb) {
+    const int b = t % NBUF;
+    const char* qt = qs[b] + t_off;
+    const char* ot = dos[b] + t_off;
+    auto c_op = [&](int j) {
       const int h = j / (NM / 2), db = (j % (NM / 2)) >> 1;
       return tr_operand<D>((j & 1) ? qt : ot, sb * 32 + 16 * h, db * 32);
     };
-    auto phaseC = [&](int sb, int other) {
-      u32x4 ring[PFC];
+    u32x4 w[4];
 #pragma unroll
-      for (int j = 0; j < PFC; ++j) ring[j] = c_op(sb, j);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int k = 0; k < 4; ++k) w[k] = xch[sb][kw][k][lane];
+    u32x4 ring[PFC];
 #pragma unroll
-      for (int j = 0; j < NM; ++j) {
-        const u32x4 a = ring[j % PFC];
-        if (j + PFC < NM) ring[j % PFC] = c_op(sb, j + PFC);
-        const int h = j / (NM / 2), db = (j % (NM / 2)) >> 1;
-        if (j & 1)
-          dk[db] = mfma32(a, pds[sb][h], dk[db]);
-        else
-          dv[db] = mfma32(a, pp[sb][h], dv[db]);
-        chunk_at(other, j);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    };
-    phaseA(0, -1);
-    phaseA(1, 0);
-    phaseC(0, 1);
-    phaseC(1, -1);
+    for (int j = 0; j < PFC; ++j) ring[j] = c_op(j);
+#pragma unroll
+    for (int j = 0; j < NM; ++j) {
+      const u32x4 a = ring[j % PFC];
+      if (j + PFC < NM) ring[j % PFC] = c_op(j + PFC);
+      const int h = j / (NM / 2), db = (j % (NM / 2)) >> 1;
+      if (j & 1)
+        dk[db] = mfma32(a, w[2 + h], dk[db]);
+      else
+        dv[db] = mfma32(a, w[h], dv[db]);
+    }
   };
-
-  // Ping-pong over the two buffer sets in a rolled loop (the buffer is an
-  // index: the asm DMA is opaque to the compiler, so naming the buffers
-  // statically buys nothing, and one loop body keeps the dK/dV accumulators in
-  // the same registers on every iteration).  The next tile is fetched
-  // unconditionally (past the segment it reads zero and is never used): the
-  // loop body stays free of branches.
-  fetch(0, qs[0], dos[0], lss[0], dss[0]);
-  wait_vmem();
-  for (int q0 = 0, b = 0;; b ^= 1) {
-    __syncthreads();  // buffers b complete; buffers b^1 no longer read
-    fetch(q0 + BQ, qs[b ^ 1], dos[b ^ 1], lss[b ^ 1], dss[b ^ 1]);
-    step(qs[b], dos[b], lss[b], dss[b]);
-    // The accumulators are only MFMA C/D operands: keep them in AGPRs across
-    // the back edge, so the register allocator does not move them.
+  for (int t = 0; t < nsteps; ++t) {
+    // phase 1: sub-block 1 of the previous tile
+    if (t > 0) phaseC(t - 1, 1);
+    __syncthreads();  // end of phase 1
+    fetch(t + 2);
+    // phase 2: sub-block 0 of this tile
+    phaseC(t, 0);
+    wait_vmem_keep<PER_FETCH_C>();  // own loads of tile t+1 landed
+    __syncthreads();  // end of phase 2
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) asm volatile("" : "+a"(dk[db]), "+a"(dv[db]));
-    wait_vmem();
-    q0 += BQ;
-    if (q0 >= it.q_len) break;
   }
+  if (nsteps > 0) phaseC(nsteps - 1, 1);
+  wait_vmem();
 
   // dK = scale * dK^T, dV = dV^T: register i <-> d = db*32 + 16*(i/8) + 8g + i%8, key = lane's key.
   if (!k_ok) return;
@@ -440,8 +454,9 @@ hipError_t launch_bwd_bf16(const BwdParams& p, int head_dim, int stage, hipStrea
     else hipLaunchKernelGGL(bwd_pre_kernel<64>, grid, block, 0, s, p);
   } else if (stage == 1) {
     if (p.n_kv_items == 0) return hipSuccess;
-    if (head_dim == 128) hipLaunchKernelGGL(bwd_dkdv_kernel<128>, dim3(p.n_kv_items), block, 0, s, p);
-    else hipLaunchKernelGGL(bwd_dkdv_kernel<64>, dim3(p.n_kv_items), block, 0, s, p);
+    const dim3 block8(kDkdvThreads);
+    if (head_dim == 128) hipLaunchKernelGGL(bwd_dkdv_kernel<128>, dim3(p.n_kv_items), block8, 0, s, p);
+    else hipLaunchKernelGGL(bwd_dkdv_kernel<64>, dim3(p.n_kv_items), block8, 0, s, p);
   } else {
     if (p.n_q_items == 0) return hipSuccess;
     if (head_dim == 128) hipLaunchKernelGGL(bwd_dq_kernel<128>, dim3(p.n_q_items), block, 0, s, p);
