@@ -100,6 +100,41 @@ def cpu_baseline(w, min_seconds):
                       f"query rows against all blocks; fwd+merge+bwd fp64; {pairs} pairs/head, {spent:.1f} s"}
 
 
+# Source files whose text determines each kernel's code; a stored counter
+# measurement applies only while their hash is unchanged.
+KERNEL_SOURCES = {
+    "fwd": ["fwd_bf16.hip"],
+    "bwd_dkdv": ["bwd_bf16.hip"],
+    "bwd_dq": ["bwd_bf16.hip"],
+    "merge": ["merge.hip"],
+}
+COMMON_SOURCES = ["zl_device.h", "zl_internal.h"]
+TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic.json")
+
+
+def kernel_source_hash(kernel: str) -> str:
+    import hashlib
+    csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_01150_amd", "csrc")
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel] + COMMON_SOURCES:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic(kernel: str, workload: str):
+    """HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE (copy-calibrated)
+    for this kernel and workload, or None if absent or taken on different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = json.load(fh).get(kernel)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("workload") != workload or rec.get("src_sha256") != kernel_source_hash(kernel):
+        return None
+    return rec
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -188,6 +223,11 @@ def main():
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": kern[dom]["tflops"], "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": kern[dom]["frac"], "traffic": None},
     }
+    tr = stored_traffic(dom, w.name)
+    if tr:
+        rec["roofline"]["traffic"] = tr["fetch_bytes"] + tr["write_bytes"]
+        rec["roofline"]["traffic_detail"] = {"fetch_bytes": tr["fetch_bytes"], "write_bytes": tr["write_bytes"],
+                                             "unique_input_output_bytes": tr.get("unique_bytes")}
     if w.num_slots and avg["merge"]:
         sr = w.shard_rows()
         nb = max(w.kv_count[s] for s in range(w.num_segments) if w.kind[s] == W.SHARD)
