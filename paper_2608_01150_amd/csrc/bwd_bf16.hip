@@ -3,25 +3,26 @@
 // Three launches on one stream, no atomics (results are deterministic):
 //   1. preprocess  D_i = dO_i . O_i in fp32 for every query row and head, and
 //                  LSE_i in log2 units for the dK/dV kernel's staging.
-//   2. dK/dV       one workgroup per item = up to 128 keys (4 waves x 32) of one
-//                  head of one K/V range, looping over every query of the
-//                  owning segment in steps of 64 rows.  One key per lane:
+//   2. dK/dV       one workgroup per item = up to 128 keys of one head of one
+//                  K/V range, looping over every query of the owning segment
+//                  in steps of 64 rows.  One key per lane:
 //                    S    = Q K^T,  dP = dO V^T      MFMA (K, V in registers)
 //                    P    = exp(S - LSE_final),  dS = P (dP - D)
-//                    dV^T += dO^T P,  dK^T += Q^T dS MFMA (P, dS from registers)
+//                    dV^T += dO^T P,  dK^T += Q^T dS MFMA (P, dS as B operands)
+//                  split between producer and consumer waves (see the kernel).
 //                  LSE_final is a shard row's merged statistic, so each block's
 //                  contribution is its exact share of the whole gradient.
-//   3. dQ          one workgroup per item = up to 128 query rows (4 waves x 32)
-//                  of one head, looping over every key of every range of the
-//                  segment in steps of 64.  One query per lane:
+//   3. dQ          one workgroup per item = up to 256 query rows (8 waves x 32)
+//                  of one head, looping over every key of the segment (all of a
+//                  shard's blocks) in steps of 64.  One query per lane:
 //                    S^T = K Q^T,  dP^T = V dO^T      MFMA (Q, dO in registers)
 //                    dS^T = P^T (dP^T - D)
 //                    dQ^T += K^T dS^T                 MFMA
 //                  A shard row sums its blocks inside one item.
 // Q/dO (dK/dV) and K/V (dQ) tiles are staged row-major (padded pitch,
-// conflict-free) in double-buffered LDS by direct global-to-LDS loads issued
-// while the previous tile computes; the transposed operands (Q^T, dO^T, K^T)
-// come straight from the row-major tiles through LDS transpose reads.
+// conflict-free) in three LDS buffers by direct buffer-to-LDS loads issued
+// ahead of use; the transposed operands (Q^T, dO^T, K^T) come straight from
+// the row-major tiles through LDS transpose reads.
 
 #include <algorithm>
 
@@ -295,13 +296,23 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
 }
 
 // ------------------------------------------------------------------ dQ
+// One workgroup of 8 waves (two per SIMD, 32 query rows each) per item of up
+// to 256 query rows of one head.  A segment's K/V ranges are consecutive rows
+// of K and V, and dQ sums over all of them against the final LSE, so the item
+// streams the segment's keys [k_start, k_start + k_len) as one range: block
+// boundaries play no part in the backward.  64-key K/V tiles rotate through
+// three LDS buffers, fetched two steps ahead (waves 0-3 load K, 4-7 load V).
+constexpr int kDqThreads = 512;
+
 template <int D>
-__global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
+__global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
   constexpr int BN = kDqTileN;                  // 64 keys per step
   constexpr int PITCH = Pad<D>::PITCH;
   constexpr int TILE = BN * PITCH;
-  // Two buffers of each tile as separate objects (see the dK/dV kernel).
-  __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], vs0[TILE], vs1[TILE];
+  using Dma = TileDma<D, BN>;
+  constexpr int DMA_PER_FETCH = Dma::PER_WAVE;  // per wave and fetch (four waves share a tile)
+  // Three buffers of each tile as separate objects (see the forward kernel).
+  __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], ks2[TILE], vs0[TILE], vs1[TILE], vs2[TILE];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -309,7 +320,6 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
   const Item it = p.q_items[dispatch_item(blockIdx.x, p.n_q_items, p.xcd_chunk)];
   const int H = p.num_heads;
   const int64_t rs = (int64_t)H * D;
-  const SegRanges sr = p.seg_ranges[it.seg];
 
   // This lane's query row and its Q, dO fragments (B operands).
   const int qr = wave * 32 + ln;
@@ -323,7 +333,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
     qf[kk] = q_ok ? *reinterpret_cast<const u32x4*>(qg + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
     of[kk] = q_ok ? *reinterpret_cast<const u32x4*>(dog + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
   }
-  const float lse2 = q_ok ? p.lse[qrow] * 1.4426950408889634f : 1.0e30f;  // +big: P = 0
+  const float lse2 = q_ok ? p.lse2[qrow] : 1.0e30f;  // +big: P = 0
   const float dd = q_ok ? p.dsum[qrow] : 0.f;
   f32x16 dq[D / 32];
 #pragma unroll
@@ -333,34 +343,23 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
   const uint32_t a_off = poff<D>(perm32(ln), g * 8);
   const uint32_t t_off = tr_lane_off<D>(lane);
 
-  // Key tiles run over the segment's ranges in order; (r, kt) is the tile
-  // [cu_k[r] + kt, cu_k[r] + kt + BN) clipped to the range.
-  const int r_end = sr.kv_first + sr.kv_count;
-  auto next_tile = [&](int r, int kt, int* ro, int* kto) {
-    while (r < r_end && kt >= p.cu_k[r + 1] - p.cu_k[r]) {
-      ++r;
-      kt = 0;
-    }
-    *ro = r;
-    *kto = kt;
-  };
-  // Rows past a range's end read zero; the step masks those keys.
-  using Dma = TileDma<D, BN>;
+  // Rows past the segment's keys read zero; the step masks those keys.
+  const uint16_t* kg = static_cast<const uint16_t*>(p.k) + ((int64_t)it.k_start * H + it.head) * D;
+  const uint16_t* vg = static_cast<const uint16_t*>(p.v) + ((int64_t)it.k_start * H + it.head) * D;
+  const bool loads_k = wave < 4;
+  const uint16_t* src0 = loads_k ? kg : vg;
   const uint32_t row_bytes = (uint32_t)rs * 2u;
   Dma dma;
-  dma.init(wave, lane, row_bytes);
-  auto fetch = [&](int r, int kt, char* kdst, char* vdst) {
-    const int k0 = p.cu_k[r] + kt, nvalid = p.cu_k[r + 1] - k0;
-    const uint16_t* kb_ = static_cast<const uint16_t*>(p.k) + ((int64_t)k0 * H + it.head) * D;
-    const uint16_t* vb_ = static_cast<const uint16_t*>(p.v) + ((int64_t)k0 * H + it.head) * D;
-    dma.issue(kdst, kb_, nvalid, row_bytes);
-    dma.issue(vdst, vb_, nvalid, row_bytes);
+  dma.init(wave & 3, lane, row_bytes);
+  auto fetch = [&](int kt, char* kdst, char* vdst) {
+    dma.issue(loads_k ? kdst : vdst, src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
   };
 
-  auto step = [&](const char* kbuf, const char* vbuf, int nvalid) {
+  auto step = [&](const char* kbuf, const char* vbuf, int kt) {
     const char* ka = kbuf + a_off;
     const char* va = vbuf + a_off;
     const char* kt_ = kbuf + t_off;
+    const int nvalid = it.k_len - kt;
     // S^T and dP^T for keys [kb*32, kb*32+32): D row m <-> key kb*32 + perm32(m).
     u32x4 pds[2][2];
 #pragma unroll
@@ -375,7 +374,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
       float e[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i) e[i] = fast_exp2(fmaf(s[i], p.scale_log2, -lse2)) * (dp[i] - dd);
-      if (nvalid < BN) {  // partial last tile of a range: keys past it contribute nothing
+      if (nvalid < BN) {  // partial last tile: keys past the segment contribute nothing
 #pragma unroll
         for (int i = 0; i < 16; ++i)
           if (kb * 32 + 16 * (i >> 3) + 8 * g + (i & 7) >= nvalid) e[i] = 0.f;
@@ -395,35 +394,31 @@ __global__ __launch_bounds__(NT, 2) void bwd_dq_kernel(BwdParams p) {
     }
   };
 
-  // Ping-pong over the two buffer sets, unrolled by two.  The next tile is
-  // fetched unconditionally: after the last one the current tile is reloaded
-  // into the idle buffer (never read).
-  int r, kt;
-  next_tile(sr.kv_first, 0, &r, &kt);
-  if (r < r_end) {
-    fetch(r, kt, ks0, vs0);
-    wait_vmem();
-    for (;;) {
-      int rn, ktn;
-      __syncthreads();  // buffers 0 complete; buffers 1 no longer read
-      next_tile(r, kt + BN, &rn, &ktn);
-      bool more = rn < r_end;
-      fetch(more ? rn : r, more ? ktn : kt, ks1, vs1);
-      step(ks0, vs0, p.cu_k[r + 1] - p.cu_k[r] - kt);
-      wait_vmem();
-      if (!more) break;
-      r = rn;
-      kt = ktn;
-      __syncthreads();  // buffers 1 complete; buffers 0 no longer read
-      next_tile(r, kt + BN, &rn, &ktn);
-      more = rn < r_end;
-      fetch(more ? rn : r, more ? ktn : kt, ks0, vs0);
-      step(ks1, vs1, p.cu_k[r + 1] - p.cu_k[r] - kt);
-      wait_vmem();
-      if (!more) break;
-      r = rn;
-      kt = ktn;
+  // Three buffer sets in rotation, unrolled by three, as in the forward.
+  if (it.k_len > 0) {
+    fetch(0, ks0, vs0);
+    fetch(BN, ks1, vs1);
+    for (int kt = 0;;) {
+      wait_vmem_keep<DMA_PER_FETCH>();
+      __syncthreads();  // tile in buffers 0 complete; buffers 2 no longer read
+      fetch(kt + 2 * BN, ks2, vs2);
+      step(ks0, vs0, kt);
+      kt += BN;
+      if (kt >= it.k_len) break;
+      wait_vmem_keep<DMA_PER_FETCH>();
+      __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
+      fetch(kt + 2 * BN, ks0, vs0);
+      step(ks1, vs1, kt);
+      kt += BN;
+      if (kt >= it.k_len) break;
+      wait_vmem_keep<DMA_PER_FETCH>();
+      __syncthreads();  // tile in buffers 2 complete; buffers 1 no longer read
+      fetch(kt + 2 * BN, ks1, vs1);
+      step(ks2, vs2, kt);
+      kt += BN;
+      if (kt >= it.k_len) break;
     }
+    wait_vmem();  // the lookahead loads must land before the workgroup's LDS is released
   }
 
   // dq[db][i] is (d = db*32 + 16*(i/8) + 8g + i%8, query qr).
@@ -459,8 +454,9 @@ hipError_t launch_bwd_bf16(const BwdParams& p, int head_dim, int stage, hipStrea
     else hipLaunchKernelGGL(bwd_dkdv_kernel<64>, dim3(p.n_kv_items), block8, 0, s, p);
   } else {
     if (p.n_q_items == 0) return hipSuccess;
-    if (head_dim == 128) hipLaunchKernelGGL(bwd_dq_kernel<128>, dim3(p.n_q_items), block, 0, s, p);
-    else hipLaunchKernelGGL(bwd_dq_kernel<64>, dim3(p.n_q_items), block, 0, s, p);
+    const dim3 block8(kDqThreads);
+    if (head_dim == 128) hipLaunchKernelGGL(bwd_dq_kernel<128>, dim3(p.n_q_items), block8, 0, s, p);
+    else hipLaunchKernelGGL(bwd_dq_kernel<64>, dim3(p.n_q_items), block8, 0, s, p);
   }
   return hipGetLastError();
 }

@@ -170,7 +170,7 @@ std::vector<zl::Item> build_items(const zl_seg_desc* d, int32_t H, int op, TileC
     const bool shard = d->kind[s] == ZL_SHARD;
     if (op == ZL_OP_BWD_DQ) {
       const int32_t j0 = d->kv_first[s], j1 = j0 + d->kv_count[s];
-      // the segment's ranges are consecutive, so their keys total cu_k[j1] - cu_k[j0]
+      // consecutive ranges are contiguous rows of K/V: the dQ item streams rows [cu_k[j0], cu_k[j1])
       const int32_t total = d->cu_seqlens_k[j1] - d->cu_seqlens_k[j0];
       for (int32_t h = 0; h < H; ++h)
         for (int32_t t0 = q0; t0 < q1; t0 += t.m)
@@ -235,8 +235,6 @@ struct Plan {
   int32_t n_segs = 0;
   int64_t n_units = 0;
   size_t slots_offset = 0;      // merge: slot list; backward: dQ items
-  size_t cuk_offset = 0;        // backward: cu_seqlens_k copy
-  size_t ranges_offset = 0;     // backward: per-segment ranges
 };
 
 size_t align256(size_t n) { return (n + 255) / 256 * 256; }
@@ -292,14 +290,9 @@ zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int
     p.n_items = (int32_t)kv.size();
     p.n_items2 = (int32_t)qi.size();
     p.slots_offset = align256(kv.size() * sizeof(zl::Item));
-    p.cuk_offset = p.slots_offset + align256(qi.size() * sizeof(zl::Item));
-    p.ranges_offset = p.cuk_offset + align256((size_t)(d->num_kv_ranges + 1) * sizeof(int32_t));
-    p.host.assign(p.ranges_offset + (size_t)d->num_q_segs * sizeof(zl::SegRanges), 0);
+    p.host.assign(p.slots_offset + qi.size() * sizeof(zl::Item), 0);
     if (!kv.empty()) std::memcpy(p.host.data(), kv.data(), kv.size() * sizeof(zl::Item));
     if (!qi.empty()) std::memcpy(p.host.data() + p.slots_offset, qi.data(), qi.size() * sizeof(zl::Item));
-    std::memcpy(p.host.data() + p.cuk_offset, d->cu_seqlens_k, (size_t)(d->num_kv_ranges + 1) * sizeof(int32_t));
-    zl::SegRanges* sr = reinterpret_cast<zl::SegRanges*>(p.host.data() + p.ranges_offset);
-    for (int32_t s = 0; s < d->num_q_segs; ++s) sr[s] = {d->kv_first[s], d->kv_count[s]};
   } else {
     std::vector<zl::Item> items = build_items(d, H, op, tile_cfg(dt, op));
     if (items.size() > (size_t)INT32_MAX) return fail(ZL_ERR_UNSUPPORTED, "too many work items");
@@ -524,8 +517,6 @@ zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype d
   p.n_kv_items = plan->n_items;
   p.q_items = reinterpret_cast<const zl::Item*>(base + plan->slots_offset);
   p.n_q_items = plan->n_items2;
-  p.cu_k = reinterpret_cast<const int32_t*>(base + plan->cuk_offset);
-  p.seg_ranges = reinterpret_cast<const zl::SegRanges*>(base + plan->ranges_offset);
   p.num_heads = H;
   p.total_q = sh.total_q;
   p.scale = scale;

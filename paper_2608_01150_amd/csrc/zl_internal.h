@@ -26,7 +26,7 @@ constexpr int kFwd32TileM = 64;      // fp32 forward: one query row per lane
 constexpr int kFwd32TileN = 32;
 constexpr int kBwdTileN = 128;       // dK/dV kernel: 4 waves x 32 keys per item
 constexpr int kBwdTileM = 64;        // queries per dK/dV inner step
-constexpr int kDqTileM = 128;        // dQ kernel: 4 waves x 32 query rows per item
+constexpr int kDqTileM = 256;        // dQ kernel: 8 waves x 32 query rows per item
 constexpr int kDqTileN = 64;         // keys per dQ inner step
 
 // Work-item index of workgroup `b`.  Workgroups are dispatched round-robin
@@ -80,11 +80,6 @@ struct MergeParams {
   int64_t lse_slot_stride;
 };
 
-// The K/V ranges a query segment attends to: kv_first .. kv_first+kv_count-1.
-struct SegRanges {
-  int32_t kv_first, kv_count;
-};
-
 struct BwdParams {
   const void* q;
   const void* k;
@@ -101,8 +96,6 @@ struct BwdParams {
   int32_t n_kv_items;
   const Item* q_items;         // dQ items: one query tile against every key of its segment
   int32_t n_q_items;
-  const int32_t* cu_k;         // device copy of cu_seqlens_k
-  const SegRanges* seg_ranges; // per query segment
   int32_t num_heads;
   int64_t total_q;             // Tq
   float scale;
