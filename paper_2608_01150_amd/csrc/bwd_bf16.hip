@@ -60,32 +60,31 @@ __global__ __launch_bounds__(NT) void bwd_pre_kernel(BwdParams p) {
 // ------------------------------------------------------------------ dK / dV
 // Warp-specialised: a workgroup of 8 waves takes 128 keys.  Producer wave w
 // (0-3) and consumer wave w+4 share keys 32w .. 32w+31 and run on the same
-// SIMD.  Per 64-query step, as two 32-query sub-blocks sb:
-//   producer  S = Q K^T, dP = dO V^T (MFMA, K and V in registers), then
-//             P = exp(S - LSE), dS = P (dP - D) (VALU), written to LDS as the
-//             consumer's bf16 B operands;
-//   consumer  dV^T += dO^T P, dK^T += Q^T dS (MFMA, dO^T and Q^T by
-//             transpose reads of the staged tiles).
-// Two waves per SIMD with complementary work let the hardware overlap the
-// producer's softmax with the consumer's MFMAs; each role fits in half the
-// register file.  Phases, separated by workgroup barriers:
-//   phase 1 of step t: producer A+B of (t, sb 0) | consumer C of (t-1, sb 1)
-//   phase 2 of step t: producer A+B of (t, sb 1) | consumer C of (t, sb 0)
-// Q/dO tiles rotate through three buffers: tile t+2 is fetched after the
-// barrier ending phase 1 of step t (its buffer held tile t-1, whose last
-// reader was that phase) and must land before phase 1 of step t+2.
+// SIMD.  The segment's queries are processed as 32-query sub-blocks k (two per
+// 64-query tile):
+//   A(k)  producer: S = Q K^T, dP = dO V^T (MFMA, K and V in registers)
+//   B(k)  producer: P = exp(S - LSE), dS = P (dP - D) (VALU), written to LDS
+//         as the consumer's bf16 B operands
+//   C(k)  consumer: dV^T += dO^T P, dK^T += Q^T dS (MFMA, dO^T and Q^T by
+//         transpose reads of the staged tiles)
+// Phase j (ended by a workgroup barrier) runs A(j) interleaved with B(j-1) on
+// the producer and C(j-2) on the consumer, so each SIMD always has MFMA work
+// from both waves and the producer's softmax hides under MFMAs.  Each role
+// fits in half the register file (two waves per SIMD).  Tile t (sub-blocks
+// 2t, 2t+1) is live from phase 2t to 2t+3; Q/dO tiles rotate through three
+// buffers and tile t+1 is fetched at the start of phase 2t.
 constexpr int kDkdvThreads = 512;
 
 template <int D>
 __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) {
-  constexpr int BQ = kBwdTileM;                 // 64 queries per step
+  constexpr int BQ = kBwdTileM;                 // 64 queries per tile
   constexpr int PITCH = Pad<D>::PITCH;
   constexpr int TILE = BQ * PITCH;              // bytes of one Q (or dO) tile
   constexpr int NBUF = 3;
-  constexpr int NM = D / 8;                     // MFMAs per phase and role
+  constexpr int NM = D / 8;                     // MFMAs per sub-block and role
   __shared__ __attribute__((aligned(16))) char qs[NBUF][TILE], dos[NBUF][TILE];
   __shared__ __attribute__((aligned(16))) float lss[NBUF][BQ], dss[NBUF][BQ];
-  // P/dS exchange: [sb][key group][word: P h0, P h1, dS h0, dS h1][lane].
+  // P/dS exchange: [k%2][key group][word: P h0, P h1, dS h0, dS h1][lane].
   __shared__ __attribute__((aligned(16))) u32x4 xch[2][4][4][64];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -102,7 +101,7 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
   const float* dsg = p.dsum + (int64_t)it.q_start * H + it.head;
   const int key = kw * 32 + ln;
   const bool k_ok = key < it.k_len;
-  const int nsteps = (it.q_len + BQ - 1) / BQ;
+  const int nsteps = (it.q_len + BQ - 1) / BQ;  // tiles
 
   const uint32_t a_off = poff<D>(perm32(ln), g * 8);
   const uint32_t t_off = tr_lane_off<D>(lane);
@@ -112,8 +111,8 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
   // consumers load the dO tile.  Rows past the segment read as zero (the
   // buffer range check), which adds exactly nothing to dK/dV: S = 0, dP = 0
   // and D = 0 give finite P and dS = 0, and the zero dO row cancels P in dV.
+  // Tiles past the last one are fetched as all zero and never used.
   using Dma = TileDma<D, BQ>;
-  constexpr int PER_FETCH_P = Dma::PER_WAVE + 1, PER_FETCH_C = Dma::PER_WAVE;
   const uint32_t row_bytes = (uint32_t)rs * 2u, stat_bytes = (uint32_t)H * 4u;
   Dma dma;
   dma.init(kw, lane, row_bytes);
@@ -131,7 +130,6 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
   };
 
   fetch(0);
-  fetch(1);
 
   if (producer) {
     // ---------------------------------------------------------- producer
@@ -143,81 +141,96 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
       kf[kk] = k_ok ? *reinterpret_cast<const u32x4*>(kg + key * rs + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
       vf[kk] = k_ok ? *reinterpret_cast<const u32x4*>(vg + key * rs + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
     }
-    // Retire the fragment loads (and with them the two tile fetches issued
-    // before) with a waitcnt the compiler sees, so the loop carries no
-    // pending register loads and gets no vmcnt wait of the compiler's.
+    // Retire the fragment loads (and tile 0) with a waitcnt the compiler
+    // sees, so the loop carries no pending register loads.
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // tile 0 published
 
     constexpr int PFA = 4;
-    for (int t = 0; t < nsteps; ++t) {
-      const int b = t % NBUF;
-      const char* qa = qs[b] + a_off;
-      const char* oa = dos[b] + a_off;
-      const float* ls = lss[b];
-      const float* ds = dss[b];
+    // S and dP of sub-block k live in sc[k%2], dp[k%2]; register i <-> query
+    // 32*(k%2) + 16*(i/8) + 8g + i%8 of tile k/2, lane = key.
+    f32x16 sc[2], dp[2];
+    // A(k) interleaved with B(k-1) (has_b); the A operand j is the Q (even j)
+    // or dO (odd j) chunk j/2 of the sub-block's 32 rows.
+    auto phase = [&](int k, bool has_b, int xb) {
+      const int ka = k & 1;
+      const int b = (k >> 1) % NBUF;
+      const char* qa = qs[b] + a_off + 32 * ka * PITCH;
+      const char* oa = dos[b] + a_off + 32 * ka * PITCH;
+      auto a_op = [&](int j) { return *reinterpret_cast<const u32x4*>(((j & 1) ? oa : qa) + poff<D>(0, (j >> 1) * 16)); };
+      const int kb = max(k - 1, 0), sbb = kb & 1, bb = (kb >> 1) % NBUF;  // B's sub-block and tile buffer
+      f32x4 lsv[2][2], dsv[2][2];
+      u32x4 pp[2], pds[2];
+      u32x4 ring[PFA];
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        // A: S and dP of the sub-block; register i <-> query sb*32 + 16*(i/8) + 8g + i%8.
-        auto a_op = [&](int j) {
-          return *reinterpret_cast<const u32x4*>(((j & 1) ? oa : qa) + poff<D>(sb * 32, (j >> 1) * 16));
-        };
-        f32x16 sc = f32x16{}, dp = f32x16{};
-        u32x4 ring[PFA];
-#pragma unroll
-        for (int j = 0; j < PFA; ++j) ring[j] = a_op(j);
-        f32x4 lsv[2][2], dsv[2][2];
+      for (int j = 0; j < PFA; ++j) ring[j] = a_op(j);
+      if (has_b) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
 #pragma unroll
           for (int e = 0; e < 2; ++e) {
-            const int q4 = sb * 32 + 16 * h + 8 * g + 4 * e;
-            lsv[h][e] = *reinterpret_cast<const f32x4*>(&ls[q4]);
-            dsv[h][e] = *reinterpret_cast<const f32x4*>(&ds[q4]);
+            const int q4 = sbb * 32 + 16 * h + 8 * g + 4 * e;
+            lsv[h][e] = *reinterpret_cast<const f32x4*>(&lss[bb][q4]);
+            dsv[h][e] = *reinterpret_cast<const f32x4*>(&dss[bb][q4]);
           }
-        }
-#pragma unroll
-        for (int j = 0; j < NM; ++j) {
-          const u32x4 a = ring[j % PFA];
-          if (j + PFA < NM) ring[j % PFA] = a_op(j + PFA);
-          if (j & 1)
-            dp = mfma32(a, vf[j >> 1], dp);
-          else
-            sc = mfma32(a, kf[j >> 1], sc);
-        }
-        // B: P = exp(S - LSE), dS = P (dP - D), packed bf16 (k = queries 16h + 8g ..).
-        // A key past the range (k_ok false) only feeds its own dK/dV, never stored.
-        u32x4 pp[2], pds[2];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-#pragma unroll
-          for (int t2 = 0; t2 < 4; ++t2) {
-            float pv[2], dv_[2];
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-              const int tt = 2 * t2 + e, i = 8 * h + tt;
-              const float l2 = lsv[h][tt >> 2][tt & 3];
-              const float dd = dsv[h][tt >> 2][tt & 3];
-              pv[e] = fast_exp2(fmaf(sc[i], p.scale_log2, -l2));
-              dv_[e] = pv[e] * (dp[i] - dd);
-            }
-            pp[h][t2] = pack_bf16(pv[0], pv[1]);
-            pds[h][t2] = pack_bf16(dv_[0], dv_[1]);
-          }
-        }
-        xch[sb][kw][0][lane] = pp[0];
-        xch[sb][kw][1][lane] = pp[1];
-        xch[sb][kw][2][lane] = pds[0];
-        xch[sb][kw][3][lane] = pds[1];
-        if (sb == 0) {
-          __syncthreads();  // end of phase 1: P/dS of sub-block 0 published
-          fetch(t + 2);     // into the buffer of tile t-1, whose last reader was phase 1
-        } else {
-          wait_vmem_keep<PER_FETCH_P>();  // own loads of tile t+1 landed
-          __syncthreads();  // end of phase 2: P/dS of sub-block 1 and tile t+1 published
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
+      f32x16 s = f32x16{}, d_ = f32x16{};
+#pragma unroll
+      for (int j = 0; j < NM; ++j) {
+        const u32x4 a = ring[j % PFA];
+        if (j + PFA < NM) ring[j % PFA] = a_op(j + PFA);
+        if (j & 1)
+          d_ = mfma32(a, vf[j >> 1], d_);
+        else
+          s = mfma32(a, kf[j >> 1], s);
+        // Chunk c = j/(NM/8) of B(k-1): elements 2c, 2c+1 -> one packed word
+        // of P and of dS.  A key past the range (k_ok false) only feeds its
+        // own dK/dV, never stored.
+        if (has_b && (j % (NM / 8)) == NM / 8 - 1) {
+          const int c = j / (NM / 8), h = c >> 2, t2 = c & 3;
+          float pv[2], dv_[2];
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const int tt = 2 * t2 + e, i = 8 * h + tt;
+            const float l2 = lsv[h][tt >> 2][tt & 3];
+            const float dd = dsv[h][tt >> 2][tt & 3];
+            pv[e] = fast_exp2(fmaf(sc[1 - ka][i], p.scale_log2, -l2));
+            dv_[e] = pv[e] * (dp[1 - ka][i] - dd);
+          }
+          pp[h][t2] = pack_bf16(pv[0], pv[1]);
+          pds[h][t2] = pack_bf16(dv_[0], dv_[1]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // S and dP are read by the VALU in the next phase: move them to arch
+      // VGPRs once, here, so they never share AGPRs with other MFMA results.
+      asm volatile("" : "+v"(s), "+v"(d_));
+      sc[ka] = s;
+      dp[ka] = d_;
+      if (has_b) {
+        xch[xb][kw][0][lane] = pp[0];
+        xch[xb][kw][1][lane] = pp[1];
+        xch[xb][kw][2][lane] = pds[0];
+        xch[xb][kw][3][lane] = pds[1];
+      }
+    };
+    // Phase 0: A(0).  Phases 2t+1, 2t+2: A(2t+1)+B(2t), A(2t+2)+B(2t+1) (the
+    // last A reads an all-zero tile past the end and is never used).  Phase
+    // 2n+1: the consumer's last sub-block.
+    fetch(1);
+    phase(0, false, 0);
+    __syncthreads();
+    for (int t = 0; t < nsteps; ++t) {
+      phase(2 * t + 1, true, 0);
+      wait_vmem();  // own loads of tile t+1 landed
+      __syncthreads();
+      fetch(t + 2);
+      phase(2 * t + 2, true, 1);
+      __syncthreads();
     }
+    __syncthreads();
     wait_vmem();  // the lookahead loads must land before the workgroup's LDS is released
     return;
   }
@@ -229,13 +242,14 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
     dk[db] = f32x16{};
     dv[db] = f32x16{};
   }
-  wait_vmem_keep<PER_FETCH_C>();  // tile 0 landed (own loads)
-  __syncthreads();                // tile 0 published
+  wait_vmem();  // tile 0 landed (own loads)
+  __syncthreads();  // tile 0 published
 
   constexpr int PFC = 3;
-  // C(sb) of tile t: operand j -> h = j / (NM/2), db = (j % (NM/2)) / 2; even j
-  // dO^T (dV), odd j Q^T (dK); A row m <-> d = db*32 + perm32(m), k <-> queries.
-  auto phaseC = [&](int t, int sb) {
+  // C(k): sub-block k = 2t + sb of tile t, P/dS from exchange buffer xb.
+  // Operand j -> h = j / (NM/2), db = (j % (NM/2)) / 2; even j dO^T (dV), odd j
+  // Q^T (dK); A row m <-> d = db*32 + perm32(m), k <-> queries.
+  auto phaseC = [&](int t, int sb, int xb) {
     const int b = t % NBUF;
     const char* qt = qs[b] + t_off;
     const char* ot = dos[b] + t_off;
@@ -245,7 +259,7 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
     };
     u32x4 w[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) w[k] = xch[sb][kw][k][lane];
+    for (int k = 0; k < 4; ++k) w[k] = xch[xb][kw][k][lane];
     u32x4 ring[PFC];
 #pragma unroll
     for (int j = 0; j < PFC; ++j) ring[j] = c_op(j);
@@ -260,20 +274,21 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
         dv[db] = mfma32(a, w[h], dv[db]);
     }
   };
+  // Phases 0, 1: nothing to consume yet.  Phases 2t+2, 2t+3: C(2t), C(2t+1).
+  fetch(1);
+  __syncthreads();
+  wait_vmem();  // own loads of tile 1 landed
+  __syncthreads();
   for (int t = 0; t < nsteps; ++t) {
-    // phase 1: sub-block 1 of the previous tile
-    if (t > 0) phaseC(t - 1, 1);
-    __syncthreads();  // end of phase 1
     fetch(t + 2);
-    // phase 2: sub-block 0 of this tile
-    phaseC(t, 0);
-    wait_vmem_keep<PER_FETCH_C>();  // own loads of tile t+1 landed
-    __syncthreads();  // end of phase 2
+    phaseC(t, 0, 0);
+    __syncthreads();
+    phaseC(t, 1, 1);
+    wait_vmem();  // own loads of tile t+2 landed
+    __syncthreads();
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) asm volatile("" : "+a"(dk[db]), "+a"(dv[db]));
   }
-  if (nsteps > 0) phaseC(nsteps - 1, 1);
-  wait_vmem();
 
   // dK = scale * dK^T, dV = dV^T: register i <-> d = db*32 + 16*(i/8) + 8g + i%8, key = lane's key.
   if (!k_ok) return;
