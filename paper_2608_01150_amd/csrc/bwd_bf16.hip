@@ -58,14 +58,15 @@ __global__ __launch_bounds__(NT) void bwd_pre_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------------ dK / dV
-// Warp-specialised: a workgroup of 8 waves takes 128 keys.  Producer wave w
-// (0-3) and consumer wave w+4 share keys 32w .. 32w+31 and run on the same
-// SIMD.  The segment's queries are processed as 32-query sub-blocks k (two per
-// 64-query tile):
+// Warp-specialised: a workgroup of 8 waves takes 128 keys, as four key groups
+// of 32.  Producer wave w (0-3) holds key group w; consumer waves 4-7 each
+// hold two key groups' dV or dK accumulators (see the consumer), and every
+// SIMD runs one producer and one consumer.  The segment's queries are
+// processed as 32-query sub-blocks k (two per 64-query tile):
 //   A(k)  producer: S = Q K^T, dP = dO V^T (MFMA, K and V in registers)
 //   B(k)  producer: P = exp(S - LSE), dS = P (dP - D) (VALU), written to LDS
 //         as the consumer's bf16 B operands
-//   C(k)  consumer: dV^T += dO^T P, dK^T += Q^T dS (MFMA, dO^T and Q^T by
+//   C(k)  consumers: dV^T += dO^T P, dK^T += Q^T dS (MFMA, dO^T and Q^T by
 //         transpose reads of the staged tiles)
 // Phase j (ended by a workgroup barrier) runs A(j) interleaved with B(j-1) on
 // the producer and C(j-2) on the consumer, so each SIMD always has MFMA work
@@ -236,42 +237,44 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
   }
 
   // ------------------------------------------------------------ consumer
-  f32x16 dk[D / 32], dv[D / 32];
+  // Consumer wave 4 + 2*kp + o owns key groups 2kp, 2kp+1 (64 keys) and one
+  // output: dV (o = 0) or dK (o = 1).  Every transpose-read operand (dO^T or
+  // Q^T) then feeds two MFMAs, one per key group.
+  const int ci = wave - 4, kp = ci >> 1;
+  const bool is_dk = (ci & 1) != 0;
+  f32x16 acc[2][D / 32];
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db) {
-    dk[db] = f32x16{};
-    dv[db] = f32x16{};
+  for (int k2 = 0; k2 < 2; ++k2) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) acc[k2][db] = f32x16{};
   }
   wait_vmem();  // tile 0 landed (own loads)
   __syncthreads();  // tile 0 published
 
   constexpr int PFC = 3;
-  // C(k): sub-block k = 2t + sb of tile t, P/dS from exchange buffer xb.
-  // Operand j -> h = j / (NM/2), db = (j % (NM/2)) / 2; even j dO^T (dV), odd j
-  // Q^T (dK); A row m <-> d = db*32 + perm32(m), k <-> queries.
+  // C(k): sub-block k = 2t + sb of tile t, P or dS from exchange buffer xb.
+  // Operand j -> h = j / (D/32), db = j % (D/32): rows of dO^T (dV) or Q^T
+  // (dK); A row m <-> d = db*32 + perm32(m), k <-> queries 16h + 8g ...
+  constexpr int NOP = 2 * (D / 32);
   auto phaseC = [&](int t, int sb, int xb) {
-    const int b = t % NBUF;
-    const char* qt = qs[b] + t_off;
-    const char* ot = dos[b] + t_off;
-    auto c_op = [&](int j) {
-      const int h = j / (NM / 2), db = (j % (NM / 2)) >> 1;
-      return tr_operand<D>((j & 1) ? qt : ot, sb * 32 + 16 * h, db * 32);
-    };
-    u32x4 w[4];
+    const char* tbuf = (is_dk ? qs[t % NBUF] : dos[t % NBUF]) + t_off;
+    auto c_op = [&](int j) { return tr_operand<D>(tbuf, sb * 32 + 16 * (j / (D / 32)), (j % (D / 32)) * 32); };
+    u32x4 w[2][2];  // [key group][h]
 #pragma unroll
-    for (int k = 0; k < 4; ++k) w[k] = xch[xb][kw][k][lane];
+    for (int k2 = 0; k2 < 2; ++k2) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) w[k2][h] = xch[xb][2 * kp + k2][(is_dk ? 2 : 0) + h][lane];
+    }
     u32x4 ring[PFC];
 #pragma unroll
     for (int j = 0; j < PFC; ++j) ring[j] = c_op(j);
 #pragma unroll
-    for (int j = 0; j < NM; ++j) {
+    for (int j = 0; j < NOP; ++j) {
       const u32x4 a = ring[j % PFC];
-      if (j + PFC < NM) ring[j % PFC] = c_op(j + PFC);
-      const int h = j / (NM / 2), db = (j % (NM / 2)) >> 1;
-      if (j & 1)
-        dk[db] = mfma32(a, w[2 + h], dk[db]);
-      else
-        dv[db] = mfma32(a, w[h], dv[db]);
+      if (j + PFC < NOP) ring[j % PFC] = c_op(j + PFC);
+      const int h = j / (D / 32), db = j % (D / 32);
+      acc[0][db] = mfma32(a, w[0][h], acc[0][db]);
+      acc[1][db] = mfma32(a, w[1][h], acc[1][db]);
     }
   };
   // Phases 0, 1: nothing to consume yet.  Phases 2t+2, 2t+3: C(2t), C(2t+1).
@@ -287,25 +290,31 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
     wait_vmem();  // own loads of tile t+2 landed
     __syncthreads();
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) asm volatile("" : "+a"(dk[db]), "+a"(dv[db]));
+    for (int k2 = 0; k2 < 2; ++k2) {
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) asm volatile("" : "+a"(acc[k2][db]));
+    }
   }
 
-  // dK = scale * dK^T, dV = dV^T: register i <-> d = db*32 + 16*(i/8) + 8g + i%8, key = lane's key.
-  if (!k_ok) return;
-  uint16_t* dkg = static_cast<uint16_t*>(p.dk) + ((int64_t)(it.k_start + key) * H + it.head) * D;
-  uint16_t* dvg = static_cast<uint16_t*>(p.dv) + ((int64_t)(it.k_start + key) * H + it.head) * D;
+  // dK = scale * dK^T or dV = dV^T: register i <-> d = db*32 + 16*(i/8) + 8g + i%8,
+  // key = key group's lane key.
+  const float osc = is_dk ? p.scale : 1.f;
+  uint16_t* og = static_cast<uint16_t*>(is_dk ? p.dk : p.dv);
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db) {
+  for (int k2 = 0; k2 < 2; ++k2) {
+    const int okey = (2 * kp + k2) * 32 + ln;
+    if (okey >= it.k_len) continue;
+    uint16_t* dst = og + ((int64_t)(it.k_start + okey) * H + it.head) * D;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      u32x4 wk, wv;
+    for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        wk[t] = pack_bf16(dk[db][8 * h + 2 * t] * p.scale, dk[db][8 * h + 2 * t + 1] * p.scale);
-        wv[t] = pack_bf16(dv[db][8 * h + 2 * t], dv[db][8 * h + 2 * t + 1]);
+      for (int h = 0; h < 2; ++h) {
+        u32x4 wo;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          wo[t] = pack_bf16(acc[k2][db][8 * h + 2 * t] * osc, acc[k2][db][8 * h + 2 * t + 1] * osc);
+        *reinterpret_cast<u32x4*>(dst + db * 32 + 16 * h + 8 * g) = wo;
       }
-      *reinterpret_cast<u32x4*>(dkg + db * 32 + 16 * h + 8 * g) = wk;
-      *reinterpret_cast<u32x4*>(dvg + db * 32 + 16 * h + 8 * g) = wv;
     }
   }
 }
