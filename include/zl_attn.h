@@ -131,6 +131,38 @@ zl_status zl_attn_fwd(const zl_seg_desc* desc, int32_t num_heads, int32_t head_d
                       void* out, float* lse, float* o_part, float* lse_part, int32_t num_slots,
                       void* stream);
 
+/* Flags of zl_attn_fwd_step. */
+#define ZL_STEP_FIRST 1u /* this call carries every SHARD row's first block */
+#define ZL_STEP_LAST 2u  /* this call carries every SHARD row's last block */
+
+/*
+ * One step of ring attention (Sec. II-B; the ring primitive (1,1,k) of
+ * Tab. II) with the output accumulation fused into the forward epilogue, so
+ * no per-block partials are stored and no merge kernel runs.  Every SHARD
+ * segment carries exactly one K/V range in this call (kv_count == 1), the
+ * block the ring delivers at this step; WHOLE segments (fillers) may ride
+ * along in any step and are computed exactly as by zl_attn_fwd.  With O_b,
+ * LSE_b the attention of SHARD row i over this call's block:
+ *   ZL_STEP_FIRST:  (o_acc, lse_acc)[i,h] = (O_b, LSE_b)
+ *   otherwise:      M = max(lse_acc, LSE_b), a = exp(lse_acc - M),
+ *                   b = exp(LSE_b - M), o_acc = (a o_acc + b O_b) / (a + b),
+ *                   lse_acc = M + ln(a + b)   (both -inf: O = 0, LSE = -inf)
+ *   ZL_STEP_LAST:   the combined result goes to out (rounded to `dtype`) and
+ *                   lse instead of o_acc / lse_acc.
+ * o_acc [Tq,H,d] fp32 and lse_acc [Tq,H] fp32 are caller-owned, indexed by
+ * packed query row like out/lse; only SHARD rows are read or written, and
+ * they may be NULL when there are no SHARD rows or when flags is
+ * ZL_STEP_FIRST|ZL_STEP_LAST.  Without ZL_STEP_FIRST they must hold the
+ * previous step's result.  block_index and num_slots are not used.  Calls
+ * for different steps must be ordered on the stream (the accumulator is
+ * read-modify-written).  Errors as zl_attn_fwd, plus ZL_ERR_INVALID_ARG for
+ * a SHARD segment with kv_count != 1 or unknown flags.
+ */
+zl_status zl_attn_fwd_step(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
+                           float softmax_scale, const void* q, const void* k, const void* v,
+                           void* out, float* lse, float* o_acc, float* lse_acc, uint32_t flags,
+                           void* stream);
+
 /*
  * LSE merge of shard partials into exact attention (the ring's output
  * accumulation, Sec. II-B).  For every SHARD row i and head h, over the slots

@@ -21,6 +21,7 @@ ZL_OK, ZL_ERR_INVALID_ARG, ZL_ERR_UNSUPPORTED, ZL_ERR_WORKSPACE, ZL_ERR_HIP = ra
 ZL_WHOLE, ZL_SHARD = 0, 1
 ZL_BF16, ZL_FP32 = 0, 1
 ZL_OP_FWD, ZL_OP_BWD, ZL_OP_BWD_DQ = 0, 1, 2
+ZL_STEP_FIRST, ZL_STEP_LAST = 1, 2
 
 
 class ZlError(RuntimeError):
@@ -74,6 +75,8 @@ _workspace_size = _sig("zl_workspace_size", ctypes.c_int, _DP, ctypes.c_int32, c
                        ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t))
 _fwd = _sig("zl_attn_fwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
             _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp)
+_fwd_step = _sig("zl_attn_fwd_step", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
+                 _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_uint32, _vp)
 _merge = _sig("zl_lse_merge", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, _vp, _vp,
               ctypes.c_int32, _vp, _vp, _vp)
 _bwd = _sig("zl_attn_bwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
@@ -222,6 +225,16 @@ def attn_fwd(desc: SegDesc, q, k, v, scale: float, out=None, lse=None, o_part=No
     _check(_fwd(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
                 _p(o_part), _p(lse_part), desc.num_slots, _stream(dev)))
     return out, lse, o_part, lse_part
+
+
+def attn_fwd_step(desc: SegDesc, q, k, v, scale: float, out, lse, o_acc, lse_acc, flags: int):
+    """zl_attn_fwd_step: one ring step; SHARD rows fold this call's block into (o_acc, lse_acc), and with
+    ZL_STEP_LAST write the final out / lse.  Every tensor is caller-provided (o_acc / lse_acc may be None only
+    when no SHARD rows need them)."""
+    tq, h, d = q.shape
+    _check(_fwd_step(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
+                     _p(o_acc), _p(lse_acc), int(flags), _stream(q.device)))
+    return out, lse
 
 
 def lse_merge(desc: SegDesc, o_part, lse_part, out, lse):

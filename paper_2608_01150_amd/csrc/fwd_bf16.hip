@@ -205,6 +205,38 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       }
     }
     if (g == 0) p.lse[row] = lse;
+  } else if (p.step_mode) {
+    // Ring step: fold this block (O_b = o * inv, LSE_b = lse) into the
+    // running accumulator; the last step writes the final output instead.
+    float* acc = p.o_acc + row * D;
+    float wa, wb, lse_new;
+    step_weights(p.step_first, p.step_first ? 0.f : p.lse_acc[row], lse, wa, wb, lse_new);
+    wb *= inv;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int c0 = db * 32 + 16 * h + 8 * g;
+        f32x4 a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
+        if (!p.step_first) {
+          a = *reinterpret_cast<const f32x4*>(acc + c0);
+          b = *reinterpret_cast<const f32x4*>(acc + c0 + 4);
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          a[t] = wa * a[t] + wb * o[db][8 * h + t];
+          b[t] = wa * b[t] + wb * o[db][8 * h + 4 + t];
+        }
+        if (p.step_last) {
+          u32x4 w = {pack_bf16(a[0], a[1]), pack_bf16(a[2], a[3]), pack_bf16(b[0], b[1]), pack_bf16(b[2], b[3])};
+          *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.out) + row * D + c0) = w;
+        } else {
+          *reinterpret_cast<f32x4*>(acc + c0) = a;
+          *reinterpret_cast<f32x4*>(acc + c0 + 4) = b;
+        }
+      }
+    }
+    if (g == 0) (p.step_last ? p.lse : p.lse_acc)[row] = lse_new;
   } else {
     float* og = p.o_part + it.slot * p.slot_stride + row * D;
 #pragma unroll

@@ -64,6 +64,24 @@ __global__ __launch_bounds__(BM) void fwd_fp32_kernel(FwdParams p) {
   const float inv = l > 0.f ? 1.f / l : 0.f;
   const float lse = l > 0.f ? m + logf(l) : -INFINITY;
   const int64_t row = (int64_t)(it.q_start + tid) * p.num_heads + it.head;
+  if (it.slot >= 0 && p.step_mode) {
+    // Ring step: fold this block into the running accumulator (see the bf16 kernel).
+    float* acc = p.o_acc + row * D;
+    float wa, wb, lse_new;
+    step_weights(p.step_first, p.step_first ? 0.f : p.lse_acc[row], lse, wa, wb, lse_new);
+    wb *= inv;
+    float* og = p.step_last ? static_cast<float*>(p.out) + row * D : acc;
+#pragma unroll
+    for (int c = 0; c < D; c += 4) {
+      f32x4 a = {0.f, 0.f, 0.f, 0.f};
+      if (!p.step_first) a = *reinterpret_cast<const f32x4*>(acc + c);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) a[t] = wa * a[t] + wb * o[c + t];
+      *reinterpret_cast<f32x4*>(og + c) = a;
+    }
+    (p.step_last ? p.lse : p.lse_acc)[row] = lse_new;
+    return;
+  }
   float* og = it.slot < 0 ? static_cast<float*>(p.out) + row * D : p.o_part + it.slot * p.slot_stride + row * D;
 #pragma unroll
   for (int c = 0; c < D; c += 4) {

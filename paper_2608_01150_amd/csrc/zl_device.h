@@ -186,6 +186,29 @@ __device__ __forceinline__ u32x4 tr_operand(const char* lane_ptr, int k0, int co
   return u32x4{lo[0], lo[1], hi[0], hi[1]};
 }
 
+// One online merge step of ring attention: with the running statistic
+// lse_acc (unless `first`) and a new block's lse_b, the merged output is
+// a * o_acc + b * O_b and the merged statistic `lse` (natural log).  Both
+// -inf (no key seen yet) gives a = b = 0 and lse = -inf.
+__device__ __forceinline__ void step_weights(bool first, float lse_acc, float lse_b, float& a, float& b, float& lse) {
+  if (first) {
+    a = 0.f;
+    b = 1.f;
+    lse = lse_b;
+    return;
+  }
+  const float m = fmaxf(lse_acc, lse_b);
+  if (m == -INFINITY) {
+    a = b = 0.f;
+    lse = -INFINITY;
+    return;
+  }
+  const float wa = expf(lse_acc - m), wb = expf(lse_b - m), den = wa + wb;
+  a = wa / den;
+  b = wb / den;
+  lse = m + logf(den);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 

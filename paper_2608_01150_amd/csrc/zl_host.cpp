@@ -55,7 +55,10 @@ struct Shape {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_slots, Shape* out) {
+// step_mode (zl_attn_fwd_step): every SHARD segment has exactly one range and
+// block slots are not used (block_index may be NULL, num_slots is ignored).
+zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_slots, Shape* out,
+                        bool step_mode = false) {
   if (!d) return fail(ZL_ERR_INVALID_ARG, "descriptor is NULL");
   const int32_t nq = d->num_q_segs, nk = d->num_kv_ranges;
   if (nq < 0 || nk < 0) return fail(ZL_ERR_INVALID_ARG, "negative segment or range count");
@@ -63,7 +66,7 @@ zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_
     return fail(ZL_ERR_INVALID_ARG, "cu_seqlens_q / cu_seqlens_k must not be NULL");
   if (nq > 0 && (!d->kind || !d->kv_first || !d->kv_count))
     return fail(ZL_ERR_INVALID_ARG, "kind / kv_first / kv_count must not be NULL");
-  if (nk > 0 && !d->block_index) return fail(ZL_ERR_INVALID_ARG, "block_index must not be NULL");
+  if (nk > 0 && !d->block_index && !step_mode) return fail(ZL_ERR_INVALID_ARG, "block_index must not be NULL");
   if (d->cu_seqlens_q[0] != 0) return fail(ZL_ERR_INVALID_ARG, "cu_seqlens_q[0] must be 0");
   if (d->cu_seqlens_k[0] != 0) return fail(ZL_ERR_INVALID_ARG, "cu_seqlens_k[0] must be 0");
   for (int32_t s = 0; s < nq; ++s)
@@ -74,7 +77,7 @@ zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_
       return fail(ZL_ERR_INVALID_ARG, "cu_seqlens_k decreases at range %d", j);
   const int32_t nslots = d->num_slots;
   if (nslots < 0) return fail(ZL_ERR_INVALID_ARG, "num_slots is negative");
-  if (check_slots && num_slots_arg != nslots)
+  if (check_slots && !step_mode && num_slots_arg != nslots)
     return fail(ZL_ERR_INVALID_ARG, "num_slots argument (%d) differs from the descriptor's (%d)",
                 num_slots_arg, nslots);
   std::vector<int32_t> owners(nk, 0);
@@ -103,6 +106,11 @@ zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_
       if (lq > 0) sh.any_whole_rows = true;
     } else {
       if (lq > 0) sh.any_shard_rows = true;
+      if (step_mode) {
+        if (c != 1)
+          return fail(ZL_ERR_INVALID_ARG, "ring step: SHARD segment %d must use exactly one range (has %d)", s, c);
+        continue;
+      }
       for (int32_t j = f; j < f + c; ++j) {
         const int32_t b = d->block_index[j];
         if (b < 0 || b >= nslots)
@@ -127,7 +135,8 @@ zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_
   }
   for (int32_t j = 0; j < nk; ++j)
     if (owners[j] > 1) sh.ranges_single_owner = false;
-  if (sh.any_shard_rows && nslots < 1) return fail(ZL_ERR_INVALID_ARG, "SHARD rows need num_slots >= 1");
+  if (sh.any_shard_rows && nslots < 1 && !step_mode)
+    return fail(ZL_ERR_INVALID_ARG, "SHARD rows need num_slots >= 1");
   *out = sh;
   return ZL_OK;
 }
@@ -179,7 +188,7 @@ std::vector<zl::Item> build_items(const zl_seg_desc* d, int32_t H, int op, TileC
     }
     for (int32_t j = d->kv_first[s]; j < d->kv_first[s] + d->kv_count[s]; ++j) {
       const int32_t k0 = d->cu_seqlens_k[j], k1 = d->cu_seqlens_k[j + 1];
-      const int32_t slot = shard ? d->block_index[j] : -1;
+      const int32_t slot = shard ? (d->block_index ? d->block_index[j] : 0) : -1;  // ring step: slot unused, >= 0 marks SHARD
       for (int32_t h = 0; h < H; ++h) {
         if (op == ZL_OP_FWD) {
           for (int32_t t0 = q0; t0 < q1; t0 += t.m)
@@ -252,7 +261,7 @@ std::vector<int64_t> plan_key(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dt
     k.push_back(d->kv_count[s]);
   }
   for (int32_t j = 0; j <= d->num_kv_ranges; ++j) k.push_back(d->cu_seqlens_k[j]);
-  for (int32_t j = 0; j < d->num_kv_ranges; ++j) k.push_back(d->block_index[j]);
+  for (int32_t j = 0; j < d->num_kv_ranges; ++j) k.push_back(d->block_index ? d->block_index[j] : 0);
   return k;
 }
 
@@ -438,6 +447,54 @@ zl_status zl_attn_fwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype d
     return dt == ZL_BF16 ? zl::launch_fwd_bf16(p, hd, s) : zl::launch_fwd_fp32(p, hd, s);
   });
   return hip_status(e, "forward launch");
+}
+
+zl_status zl_attn_fwd_step(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
+                           const void* k, const void* v, void* out, float* lse, float* o_acc, float* lse_acc,
+                           uint32_t flags, void* stream) {
+  zl_status st = validate_common(H, hd, dt, scale, true);
+  if (st != ZL_OK) return st;
+  if (flags & ~(ZL_STEP_FIRST | ZL_STEP_LAST)) return fail(ZL_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+  Shape sh;
+  if ((st = validate_desc(desc, 0, false, &sh, true)) != ZL_OK) return st;
+  if ((st = check_sizes(sh, H, hd, 1)) != ZL_OK) return st;
+  const bool first = flags & ZL_STEP_FIRST, last = flags & ZL_STEP_LAST;
+  if (sh.total_q > 0 && !q) return fail(ZL_ERR_INVALID_ARG, "q is NULL");
+  if (sh.total_k > 0 && (!k || !v)) return fail(ZL_ERR_INVALID_ARG, "k or v is NULL");
+  if ((sh.any_whole_rows || (sh.any_shard_rows && last)) && (!out || !lse))
+    return fail(ZL_ERR_INVALID_ARG, "WHOLE rows and the last ring step need out and lse");
+  if (sh.any_shard_rows && !(first && last) && (!o_acc || !lse_acc))
+    return fail(ZL_ERR_INVALID_ARG, "SHARD rows need o_acc and lse_acc unless the call is both first and last");
+  for (const void* p : {q, k, v, (const void*)out, (const void*)o_acc})
+    if (p && !aligned(p, 16)) return fail(ZL_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  for (const void* p : {(const void*)lse, (const void*)lse_acc})
+    if (p && !aligned(p, 4)) return fail(ZL_ERR_INVALID_ARG, "LSE pointers must be 4-byte aligned");
+  std::lock_guard<std::mutex> lock(g_mu);
+  Plan* plan = nullptr;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = get_plan(desc, H, hd, dt, ZL_OP_FWD, s, &plan)) != ZL_OK) return st;
+  if (plan->n_items == 0) return ok();
+  zl::FwdParams p{};
+  p.q = q;
+  p.k = k;
+  p.v = v;
+  p.out = out;
+  p.lse = lse;
+  p.items = static_cast<const zl::Item*>(plan->dev);
+  p.n_items = plan->n_items;
+  p.num_heads = H;
+  p.scale = scale;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  p.xcd_chunk = xcd_chunk();
+  p.step_mode = 1;
+  p.step_first = first;
+  p.step_last = last;
+  p.o_acc = o_acc;
+  p.lse_acc = lse_acc;
+  hipError_t e = timed(ZL_K_FWD, s, [&] {
+    return dt == ZL_BF16 ? zl::launch_fwd_bf16(p, hd, s) : zl::launch_fwd_fp32(p, hd, s);
+  });
+  return hip_status(e, "ring-step forward launch");
 }
 
 zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype out_dt, const float* o_part,

@@ -59,6 +59,13 @@ struct FwdParams {
   float scale;           // softmax scale
   float scale_log2;      // softmax scale * log2(e)
   int32_t xcd_chunk;
+  // Ring-step mode (zl_attn_fwd_step): SHARD items fold their block into the
+  // running (o_acc, lse_acc) instead of writing a partial slot.
+  int32_t step_mode;
+  int32_t step_first;    // the accumulator starts from this block
+  int32_t step_last;     // the combined result goes to out / lse
+  float* o_acc;          // [Tq, H, d] fp32
+  float* lse_acc;        // [Tq, H] fp32
 };
 
 struct MergeSeg {

@@ -16,7 +16,7 @@ def test_exports_every_declared_symbol():
     names = api.header_symbols()
     assert {"zl_attn_fwd", "zl_attn_bwd", "zl_lse_merge", "zl_plan_dump", "zl_workspace_size",
             "zl_last_error", "zl_abi_version", "zl_shutdown", "zl_profile_enable", "zl_profile_read",
-            "zl_profile_reset"} <= set(names)
+            "zl_profile_reset", "zl_attn_fwd_step"} <= set(names)
     for n in names:
         assert hasattr(api._lib, n), n
 
@@ -99,3 +99,36 @@ def test_last_error_cleared_by_success():
     assert api.last_error()
     api.workspace_size(d, 2, 64, torch.bfloat16, api.ZL_OP_FWD)
     assert api.last_error() == ""
+
+
+def _step(d, flags=api.ZL_STEP_FIRST | api.ZL_STEP_LAST, ptrs=(FAKE,) * 7, H=2, hd=64):
+    return api._fwd_step(d.ptr(), H, hd, api.ZL_BF16, 0.125, *ptrs, flags, None)
+
+
+def _step_desc(**over):
+    """mixed_small with the 150-query shard reduced to its first block (one ring step)."""
+    base = _descs.desc(cu_q=(0, 200, 200, 277, 427, 460), kind=(0, 0, 0, 1, 1), kv_first=(0, 1, 2, 3, 4),
+                       kv_count=(1, 1, 1, 1, 1), cu_k=(0, 200, 200, 277, 577, 641), block_index=(0, 0, 0, 0, 0),
+                       num_slots=1)
+    base.update(over)
+    return api.SegDesc.of(base)
+
+
+def test_ring_step_rules():
+    # a SHARD segment must bring exactly one block per step
+    assert _step(_ok_desc()) == api.ZL_ERR_INVALID_ARG and "exactly one range" in api.last_error()
+    # unknown flags
+    assert _step(_step_desc(), flags=4) == api.ZL_ERR_INVALID_ARG and "flags" in api.last_error()
+    # without ZL_STEP_FIRST|ZL_STEP_LAST the SHARD rows need the accumulator
+    ptrs = (FAKE,) * 5 + (None, None)
+    for flags in (0, api.ZL_STEP_FIRST, api.ZL_STEP_LAST):
+        assert _step(_step_desc(), flags=flags, ptrs=ptrs) == api.ZL_ERR_INVALID_ARG
+        assert "o_acc" in api.last_error()
+    # the last step needs out / lse even with no WHOLE rows
+    only_shard = _descs.desc(cu_q=(0, 33), kind=(1,), kv_first=(0,), kv_count=(1,), cu_k=(0, 64), block_index=(0,),
+                             num_slots=1)
+    assert _step(api.SegDesc.of(only_shard), flags=api.ZL_STEP_LAST,
+                 ptrs=(FAKE, FAKE, FAKE, None, None, FAKE, FAKE)) == api.ZL_ERR_INVALID_ARG
+    # misaligned accumulator
+    assert _step(_step_desc(), flags=0, ptrs=(FAKE,) * 5 + (FAKE + 4, FAKE)) == api.ZL_ERR_INVALID_ARG
+    assert "16-byte" in api.last_error()

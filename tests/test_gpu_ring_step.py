@@ -1,0 +1,108 @@
+"""GPU parity of the ring-step forward (zl_attn_fwd_step): a shard sees one
+K/V block per call and the epilogue folds it into a running fp32 (O, LSE)
+(Sec. II-B, ring attention), with WHOLE fillers riding along in any step.
+After the last step every shard row must equal exact attention over the
+concatenation of its blocks, and every filler its own exact attention, to
+the same tolerances as the all-blocks path (bf16: max|dO| <= 2e-2,
+max|dLSE| <= 1e-3; fp32 plumbing: 1e-5)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests._gpu import HAVE_GPU, api, to64
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not HAVE_GPU, reason="needs a GPU")]
+
+O_TOL, LSE_TOL = 2e-2, 1e-3
+
+
+def _ring(shard_q, shard_blocks, fillers, fill_step, H, hd, dtype, seed):
+    """shard_q: query count per shard; shard_blocks[s]: key counts of its blocks
+    (all shards have the same number of blocks R); fillers: WHOLE lengths;
+    fill_step[f]: the step that carries filler f."""
+    R = len(shard_blocks[0])
+    g = torch.Generator().manual_seed(seed)
+    rnd = lambda n: torch.randn((n, H, hd), generator=g).to(dtype)
+    qs = [rnd(n) for n in shard_q]
+    ks = [[rnd(n) for n in bl] for bl in shard_blocks]
+    vs = [[rnd(n) for n in bl] for bl in shard_blocks]
+    fq = [rnd(n) for n in fillers]
+    fk = [rnd(n) for n in fillers]
+    fv = [rnd(n) for n in fillers]
+    scale = 1.0 / hd ** 0.5
+    n_sq = sum(shard_q)
+    max_tq = n_sq + max([sum(n for f, n in enumerate(fillers) if fill_step[f] == r) for r in range(R)] + [0])
+    dev = "cuda"
+    # a single step (FIRST|LAST) needs no accumulator: pass none
+    o_acc = torch.full((max_tq, H, hd), float("nan"), device=dev) if R > 1 else None
+    lse_acc = torch.full((max_tq, H), float("nan"), device=dev) if R > 1 else None
+    shard_out = shard_lse = None
+    fill_out = {}
+    for r in range(R):
+        fs = [f for f in range(len(fillers)) if fill_step[f] == r]
+        lq = list(shard_q) + [fillers[f] for f in fs]
+        lk = [bl[r] for bl in shard_blocks] + [fillers[f] for f in fs]
+        kinds = [1] * len(shard_q) + [0] * len(fs)
+        cu_q = np.concatenate([[0], np.cumsum(lq)]).astype(np.int32)
+        cu_k = np.concatenate([[0], np.cumsum(lk)]).astype(np.int32)
+        nseg = len(lq)
+        desc = api.SegDesc(cu_q, np.array(kinds, np.uint8), np.arange(nseg, dtype=np.int32),
+                           np.ones(nseg, np.int32), cu_k, np.zeros(nseg, np.int32), 1)
+        q = torch.cat(qs + [fq[f] for f in fs]).to(dev)
+        k = torch.cat([ks[s][r] for s in range(len(shard_q))] + [fk[f] for f in fs]).to(dev)
+        v = torch.cat([vs[s][r] for s in range(len(shard_q))] + [fv[f] for f in fs]).to(dev)
+        out = torch.full_like(q, float("nan"))
+        lse = torch.full((q.shape[0], H), float("nan"), device=dev)
+        flags = (api.ZL_STEP_FIRST if r == 0 else 0) | (api.ZL_STEP_LAST if r == R - 1 else 0)
+        api.attn_fwd_step(desc, q, k, v, scale, out, lse, o_acc, lse_acc, flags)
+        torch.cuda.synchronize()
+        row = n_sq
+        for f in fs:
+            fill_out[f] = (out[row:row + fillers[f]].clone(), lse[row:row + fillers[f]].clone())
+            row += fillers[f]
+        if r == R - 1:
+            shard_out, shard_lse = out[:n_sq].clone(), lse[:n_sq].clone()
+        # rows outside the shards are never touched in the accumulator
+        if o_acc is not None:
+            assert torch.isnan(o_acc[n_sq:]).all() and torch.isnan(lse_acc[n_sq:]).all()
+    tol_o, tol_l = (1e-5, 1e-5) if dtype == torch.float32 else (O_TOL, LSE_TOL)
+    row = 0
+    for s, n in enumerate(shard_q):
+        kk = torch.cat(ks[s]).double().numpy()
+        vv = torch.cat(vs[s]).double().numpy()
+        for h in range(H):
+            o_ref, l_ref = oracle.attend(qs[s][:, h].double().numpy(), kk[:, h], vv[:, h], scale)
+            np.testing.assert_allclose(to64(shard_out[row:row + n, h]), o_ref, rtol=0, atol=tol_o)
+            np.testing.assert_allclose(to64(shard_lse[row:row + n, h]), l_ref, rtol=0, atol=tol_l)
+        row += n
+    for f, n in enumerate(fillers):
+        o_got, l_got = fill_out[f]
+        for h in range(H):
+            o_ref, l_ref = oracle.attend(fq[f][:, h].double().numpy(), fk[f][:, h].double().numpy(),
+                                         fv[f][:, h].double().numpy(), scale)
+            np.testing.assert_allclose(to64(o_got[:, h]), o_ref, rtol=0, atol=tol_o)
+            np.testing.assert_allclose(to64(l_got[:, h]), l_ref, rtol=0, atol=tol_l)
+
+
+@pytest.mark.parametrize("hd", [64, 128])
+def test_ring_steps_bf16(hd):
+    # two shards over four blocks each (one block empty, ragged sizes), fillers in steps 0, 1, 3
+    _ring(shard_q=(150, 33), shard_blocks=((300, 0, 129, 64), (64, 191, 1, 256)), fillers=(200, 77, 1),
+          fill_step=(0, 1, 3), H=2, hd=hd, dtype=torch.bfloat16, seed=31)
+
+
+def test_ring_steps_first_block_empty_bf16():
+    _ring(shard_q=(97,), shard_blocks=((0, 130, 0),), fillers=(), fill_step=(), H=3, hd=128,
+          dtype=torch.bfloat16, seed=32)
+
+
+def test_ring_single_step_bf16():
+    # FIRST|LAST in one call: no accumulator needed at all
+    _ring(shard_q=(129,), shard_blocks=((257,),), fillers=(64,), fill_step=(0,), H=2, hd=128,
+          dtype=torch.bfloat16, seed=33)
+
+
+def test_ring_steps_fp32():
+    _ring(shard_q=(70, 5), shard_blocks=((64, 33, 0), (128, 1, 7)), fillers=(40,), fill_step=(2,), H=2, hd=64,
+          dtype=torch.float32, seed=34)
