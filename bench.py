@@ -36,6 +36,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c4", help="c2..c5 (default c4: coalesced whole+shard)")
+    ap.add_argument("--mode", default="blocks", choices=("blocks", "ring", "gather"),
+                    help="how a shard's K/V blocks reach the forward: blocks = all blocks in one launch plus "
+                         "the LSE merge (default); ring = one ring step per block with the merge fused into "
+                         "the epilogue (fillers spread over the steps); gather = one launch against the "
+                         "concatenated blocks (all-gather), no partials and no merge")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="accumulate oracle heads until this much CPU time is spent")
@@ -98,6 +103,58 @@ def cpu_baseline(w, min_seconds):
     return {"value": flops / spent / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{heads} of {w.num_heads} heads; whole segments in full, each shard's first 1/9 of "
                       f"query rows against all blocks; fwd+merge+bwd fp64; {pairs} pairs/head, {spent:.1f} s"}
+
+
+def gathered_descriptor(w):
+    """The batch with each SHARD segment's consecutive K/V ranges merged into one range (the K/V an
+    all-gather delivers): no partial slots, no merge."""
+    import numpy as np
+    cu_k = [0]
+    kv_first, kv_count, bidx = [], [], []
+    for s in range(w.num_segments):
+        j0, j1 = w.kv_first[s], w.kv_first[s] + w.kv_count[s]
+        kv_first.append(len(cu_k) - 1)
+        kv_count.append(1)
+        cu_k.append(cu_k[-1] + int(w.cu_seqlens_k[j1] - w.cu_seqlens_k[j0]))
+        bidx.append(0)
+    return dict(cu_seqlens_q=np.asarray(w.cu_seqlens_q, np.int32), kind=np.asarray(w.kind, np.uint8),
+                kv_first=np.asarray(kv_first, np.int32), kv_count=np.asarray(kv_count, np.int32),
+                cu_seqlens_k=np.asarray(cu_k, np.int32), block_index=np.asarray(bidx, np.int32), num_slots=1,
+                q_offset=None, k_offset=None)
+
+
+def ring_steps(w, q, k, v):
+    """Per-step packed inputs of the ring: step r carries block r of every shard (shard rows first, so
+    the accumulator rows line up) and the WHOLE fillers with index % R == r."""
+    import numpy as np
+    import torch
+    from paper_2608_01150_amd import api
+    from paper_2608_01150_amd import workloads as W
+    shards = [s for s in range(w.num_segments) if w.kind[s] == W.SHARD]
+    wholes = [s for s in range(w.num_segments) if w.kind[s] == W.WHOLE]
+    R = w.kv_count[shards[0]]
+    assert all(w.kv_count[s] == R for s in shards), "ring mode needs every shard to have the same block count"
+    rows = lambda s: (int(w.cu_seqlens_q[s]), int(w.cu_seqlens_q[s + 1]))
+    krows = lambda j: (int(w.cu_seqlens_k[j]), int(w.cu_seqlens_k[j + 1]))
+    n_sq = sum(b - a for a, b in map(rows, shards))
+    out = []
+    for r in range(R):
+        segs = shards + [s for i, s in enumerate(wholes) if i % R == r]
+        lq = [rows(s)[1] - rows(s)[0] for s in segs]
+        ranges = [krows(w.kv_first[s] + (r if w.kind[s] == W.SHARD else 0)) for s in segs]
+        lk = [b - a for a, b in ranges]
+        n = len(segs)
+        desc = api.SegDesc(np.concatenate([[0], np.cumsum(lq)]).astype(np.int32),
+                           np.asarray([w.kind[s] for s in segs], np.uint8), np.arange(n, dtype=np.int32),
+                           np.ones(n, np.int32), np.concatenate([[0], np.cumsum(lk)]).astype(np.int32),
+                           np.zeros(n, np.int32), 1)
+        qr = torch.cat([q[slice(*rows(s))] for s in segs])
+        kr = torch.cat([k[a:b] for a, b in ranges])
+        vr = torch.cat([v[a:b] for a, b in ranges])
+        out.append(dict(desc=desc, q=qr, k=kr, v=vr, out=torch.empty_like(qr),
+                        lse=torch.empty((qr.shape[0], q.shape[1]), dtype=torch.float32, device=q.device),
+                        n_shard_rows=n_sq))
+    return out
 
 
 # Source files whose text determines each kernel's code; a stored counter
@@ -180,6 +237,32 @@ def main():
             api.lse_merge(desc, o_part, lse_part, out, lse)
         api.attn_bwd(desc, q, k, v, out, lse, do, w.scale, dq, dk, dv, ws)
 
+    if args.mode == "gather":
+        gdesc = api.SegDesc.of(gathered_descriptor(w))
+
+        def step():
+            api.attn_fwd_step(gdesc, q, k, v, w.scale, out, lse, None, None, api.ZL_STEP_FIRST | api.ZL_STEP_LAST)
+            api.attn_bwd(gdesc, q, k, v, out, lse, do, w.scale, dq, dk, dv, ws)
+    elif args.mode == "ring":
+        steps_in = ring_steps(w, q, k, v)
+        n_sq = steps_in[0]["n_shard_rows"]
+        max_tq = max(st["q"].shape[0] for st in steps_in)
+        o_acc = torch.empty((max_tq, H, hd), dtype=torch.float32, device=dev)
+        lse_acc = torch.empty((max_tq, H), dtype=torch.float32, device=dev)
+        # the backward consumes final outputs in the packed layout; they come from an
+        # all-blocks forward made once here (the same values up to rounding)
+        api.attn_fwd(desc, q, k, v, w.scale, out, lse, o_part, lse_part)
+        if w.num_slots:
+            api.lse_merge(desc, o_part, lse_part, out, lse)
+        R = len(steps_in)
+
+        def step():
+            for r, st in enumerate(steps_in):
+                flags = (api.ZL_STEP_FIRST if r == 0 else 0) | (api.ZL_STEP_LAST if r == R - 1 else 0)
+                api.attn_fwd_step(st["desc"], st["q"], st["k"], st["v"], w.scale, st["out"], st["lse"], o_acc,
+                                  lse_acc, flags)
+            api.attn_bwd(desc, q, k, v, out, lse, do, w.scale, dq, dk, dv, ws)
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -195,7 +278,8 @@ def main():
     api.profile_enable(False)
     ms = start.elapsed_time(end) / args.steps
     kt = {name: api.profile_read(kid) for kid, name in api.KERNEL_NAMES.items()}
-    avg = {name: (t / n if n else 0.0) for name, (t, n) in kt.items()}
+    # per step (a ring step launches the forward once per block)
+    avg = {name: (t / args.steps if n else 0.0) for name, (t, n) in kt.items()}
 
     pairs = w.pair_count()
     fa_flops = 14.0 * hd * H * pairs
@@ -214,7 +298,8 @@ def main():
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": w.name, "heads": H, "head_dim": hd, "total_q": w.total_q, "total_k": w.total_k,
+        "config": {"workload": w.name, "mode": args.mode, "heads": H, "head_dim": hd, "total_q": w.total_q,
+                   "total_k": w.total_k,
                    "pairs_per_head": pairs, "shard_rows": w.shard_rows(), "num_slots": w.num_slots},
         "pct_of_mfma_peak": round(100.0 * value / BF16_PEAK_TFLOPS, 2),
         "algorithmic_tflops_12d": round(12.0 * hd * H * pairs / (ms * 1e-3) / 1e12, 2),
@@ -228,7 +313,7 @@ def main():
         rec["roofline"]["traffic"] = tr["fetch_bytes"] + tr["write_bytes"]
         rec["roofline"]["traffic_detail"] = {"fetch_bytes": tr["fetch_bytes"], "write_bytes": tr["write_bytes"],
                                              "unique_input_output_bytes": tr.get("unique_bytes")}
-    if w.num_slots and avg["merge"]:
+    if w.num_slots and avg.get("merge"):
         sr = w.shard_rows()
         nb = max(w.kv_count[s] for s in range(w.num_segments) if w.kind[s] == W.SHARD)
         mbytes = H * sr * (nb * (4 * hd + 4) + 2 * hd + 4)

@@ -106,3 +106,40 @@ def test_ring_single_step_bf16():
 def test_ring_steps_fp32():
     _ring(shard_q=(70, 5), shard_blocks=((64, 33, 0), (128, 1, 7)), fillers=(40,), fill_step=(2,), H=2, hd=64,
           dtype=torch.float32, seed=34)
+
+
+def test_all_gather_mode_matches_all_blocks_mode():
+    """All-gather mode (Tab. II (q,1,1)): each shard attends once to the concatenation of its blocks
+    (one range, zl_attn_fwd_step with FIRST|LAST): no partials, no merge.  It must agree with the
+    all-blocks launch plus LSE merge on the same inputs, and with the oracle."""
+    from tests import _descs
+    d = _descs.mixed_small()          # shard 3 has blocks of 300, 0 and 129 keys, consecutive in K
+    H, hd = 2, 128
+    g = torch.Generator().manual_seed(35)
+    tq, tk = d["cu_seqlens_q"][-1], d["cu_seqlens_k"][-1]
+    q, k, v = (torch.randn((n, H, hd), generator=g).to(torch.bfloat16) for n in (tq, tk, tk))
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    scale = 1.0 / hd ** 0.5
+    desc = api.SegDesc.of(d)
+    out_b, lse_b, op, lp = api.attn_fwd(desc, qd, kd, vd, scale)
+    api.lse_merge(desc, op, lp, out_b, lse_b)
+    # gathered descriptor: every segment keeps its consecutive ranges as one
+    cu_k, first = [0], []
+    for s in range(len(d["kind"])):
+        j0, j1 = d["kv_first"][s], d["kv_first"][s] + d["kv_count"][s]
+        first.append(len(cu_k) - 1)
+        cu_k.append(cu_k[-1] + d["cu_seqlens_k"][j1] - d["cu_seqlens_k"][j0])
+    n = len(d["kind"])
+    gdesc = api.SegDesc(np.asarray(d["cu_seqlens_q"], np.int32), np.asarray(d["kind"], np.uint8),
+                        np.asarray(first, np.int32), np.ones(n, np.int32), np.asarray(cu_k, np.int32),
+                        np.zeros(n, np.int32), 1)
+    out_g = torch.full_like(qd, float("nan"))
+    lse_g = torch.full((tq, H), float("nan"), device="cuda")
+    api.attn_fwd_step(gdesc, qd, kd, vd, scale, out_g, lse_g, None, None, api.ZL_STEP_FIRST | api.ZL_STEP_LAST)
+    torch.cuda.synchronize()
+    rows = np.arange(tq)
+    np.testing.assert_allclose(to64(out_g[rows]), to64(out_b[rows]), rtol=0, atol=O_TOL)
+    np.testing.assert_allclose(to64(lse_g[rows]), to64(lse_b[rows]), rtol=0, atol=LSE_TOL)
+    ref = oracle.packed_forward(d, q.double().numpy(), k.double().numpy(), v.double().numpy(), scale)
+    np.testing.assert_allclose(to64(out_g), ref["final_out"], rtol=0, atol=O_TOL)
+    np.testing.assert_allclose(to64(lse_g), ref["final_lse"], rtol=0, atol=LSE_TOL)
