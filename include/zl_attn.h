@@ -164,6 +164,48 @@ zl_status zl_attn_fwd_step(const zl_seg_desc* desc, int32_t num_heads, int32_t h
                            void* stream);
 
 /*
+ * Ulysses (1,h,1) local staging (Sec. II-B; Tab. II; Sec. IV-D's coalesced
+ * QKV-packed all-to-all): the layout kernels around one block-diagonal
+ * attention call on a head subset.  A group of `group` ranks each hold a
+ * token shard of every batched sequence with all num_heads heads; rank j
+ * computes heads [j*Hl, (j+1)*Hl), Hl = num_heads / group, over the full
+ * sequences.  The all-to-alls themselves are the caller's (RCCL); these calls
+ * only lay out the buffers they move.  All tensors bf16, 16-byte aligned,
+ * head_dim 64 or 128; rows of every layout are in sequence order.
+ *
+ *   zl_ulysses_pack_qkv    q, k, v [t_local, H, d] -> send [group][t_local][Hl][3][d]:
+ *                          the chunk for rank j (contiguous) holds its heads, q/k/v
+ *                          interleaved per head so one all-to-all moves all three.
+ *   zl_ulysses_unpack_qkv  recv (rank-major: rank j's T_j rows, [T_j][Hl][3][d]) ->
+ *                          q, k, v [T_full, Hl, d] in full-sequence order, ready for
+ *                          zl_attn_fwd / zl_attn_bwd with WHOLE segments of the full
+ *                          lengths and num_heads = Hl.
+ *   zl_ulysses_pack_out    out [T_full, Hl, d] -> send, rank-major ([T_j][Hl][d] for
+ *                          rank j: its shard rows of every sequence).
+ *   zl_ulysses_unpack_out  recv [group][t_local][Hl][d] (rank j's head group) ->
+ *                          out_local [t_local, H, d].
+ *
+ * cu_rank (HOST, [group][num_seqs+1], read during the call): cu_rank[j][s] is
+ * where sequence s starts among rank j's local rows (cu_rank[j][0] = 0, non-
+ * decreasing), so rank j holds T_j = cu_rank[j][num_seqs] rows and sequence s
+ * has sum_j (cu_rank[j][s+1] - cu_rank[j][s]) tokens, rank j's shard after
+ * those of ranks < j.  Shards may differ in length (all-to-all-v).  The
+ * row map it implies is cached on the device like a work table.  Errors:
+ * ZL_ERR_INVALID_ARG (group < 1, num_heads not a multiple of group, bad
+ * cu_rank, NULL or misaligned pointers), ZL_ERR_UNSUPPORTED (dtype other
+ * than bf16, head_dim), ZL_ERR_HIP; nothing is enqueued on error.
+ */
+zl_status zl_ulysses_pack_qkv(int32_t group, int32_t t_local, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
+                              const void* q, const void* k, const void* v, void* send, void* stream);
+zl_status zl_ulysses_unpack_qkv(int32_t group, int32_t num_seqs, const int32_t* cu_rank, int32_t num_heads,
+                                int32_t head_dim, zl_dtype dtype, const void* recv, void* q, void* k, void* v,
+                                void* stream);
+zl_status zl_ulysses_pack_out(int32_t group, int32_t num_seqs, const int32_t* cu_rank, int32_t num_heads,
+                              int32_t head_dim, zl_dtype dtype, const void* out, void* send, void* stream);
+zl_status zl_ulysses_unpack_out(int32_t group, int32_t t_local, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
+                                const void* recv, void* out_local, void* stream);
+
+/*
  * LSE merge of shard partials into exact attention (the ring's output
  * accumulation, Sec. II-B).  For every SHARD row i and head h, over the slots
  * B of its blocks:  M = max_b LSE_b, LSE = M + ln sum_b exp(LSE_b - M),

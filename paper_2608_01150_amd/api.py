@@ -77,6 +77,14 @@ _fwd = _sig("zl_attn_fwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ct
             _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp)
 _fwd_step = _sig("zl_attn_fwd_step", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
                  _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_uint32, _vp)
+_u_pack_qkv = _sig("zl_ulysses_pack_qkv", ctypes.c_int, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                   ctypes.c_int, _vp, _vp, _vp, _vp, _vp)
+_u_unpack_qkv = _sig("zl_ulysses_unpack_qkv", ctypes.c_int, ctypes.c_int32, ctypes.c_int32, _i32p, ctypes.c_int32,
+                     ctypes.c_int32, ctypes.c_int, _vp, _vp, _vp, _vp, _vp)
+_u_pack_out = _sig("zl_ulysses_pack_out", ctypes.c_int, ctypes.c_int32, ctypes.c_int32, _i32p, ctypes.c_int32,
+                   ctypes.c_int32, ctypes.c_int, _vp, _vp, _vp)
+_u_unpack_out = _sig("zl_ulysses_unpack_out", ctypes.c_int, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                     ctypes.c_int32, ctypes.c_int, _vp, _vp, _vp)
 _merge = _sig("zl_lse_merge", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, _vp, _vp,
               ctypes.c_int32, _vp, _vp, _vp)
 _bwd = _sig("zl_attn_bwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
@@ -235,6 +243,53 @@ def attn_fwd_step(desc: SegDesc, q, k, v, scale: float, out, lse, o_acc, lse_acc
     _check(_fwd_step(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
                      _p(o_acc), _p(lse_acc), int(flags), _stream(q.device)))
     return out, lse
+
+
+def _cu_rank(cu_rank):
+    a = np.ascontiguousarray(np.asarray(cu_rank, dtype=np.int32))
+    if a.ndim != 2:
+        raise ZlError(ZL_ERR_INVALID_ARG, "cu_rank must be [group, num_seqs + 1]")
+    return a
+
+
+def ulysses_pack_qkv(group: int, q, k, v, send=None):
+    """zl_ulysses_pack_qkv: local q, k, v [T, H, d] -> send [group, T, H/group, 3, d]."""
+    t, h, d = q.shape
+    if send is None:
+        send = torch.empty((group, t, h // group, 3, d), dtype=q.dtype, device=q.device)
+    _check(_u_pack_qkv(group, t, h, d, _dtype_code(q.dtype), _p(q), _p(k), _p(v), _p(send), _stream(q.device)))
+    return send
+
+
+def ulysses_unpack_qkv(group: int, cu_rank, recv, num_heads: int, q=None, k=None, v=None):
+    """zl_ulysses_unpack_qkv: rank-major recv [T_full, H/group, 3, d] -> q, k, v [T_full, H/group, d]."""
+    cu = _cu_rank(cu_rank)
+    tf, hl, _, d = recv.shape
+    q = torch.empty((tf, hl, d), dtype=recv.dtype, device=recv.device) if q is None else q
+    k = torch.empty_like(q) if k is None else k
+    v = torch.empty_like(q) if v is None else v
+    _check(_u_unpack_qkv(group, cu.shape[1] - 1, cu.ctypes.data_as(_i32p), num_heads, d, _dtype_code(recv.dtype),
+                         _p(recv), _p(q), _p(k), _p(v), _stream(recv.device)))
+    return q, k, v
+
+
+def ulysses_pack_out(group: int, cu_rank, out, num_heads: int, send=None):
+    """zl_ulysses_pack_out: out [T_full, H/group, d] -> rank-major send [T_full, H/group, d]."""
+    cu = _cu_rank(cu_rank)
+    send = torch.empty_like(out) if send is None else send
+    _check(_u_pack_out(group, cu.shape[1] - 1, cu.ctypes.data_as(_i32p), num_heads, out.shape[2],
+                       _dtype_code(out.dtype), _p(out), _p(send), _stream(out.device)))
+    return send
+
+
+def ulysses_unpack_out(group: int, recv, num_heads: int, out_local=None):
+    """zl_ulysses_unpack_out: recv [group, T, H/group, d] -> out_local [T, H, d]."""
+    g, t, hl, d = recv.shape
+    if out_local is None:
+        out_local = torch.empty((t, num_heads, d), dtype=recv.dtype, device=recv.device)
+    _check(_u_unpack_out(group, t, num_heads, d, _dtype_code(recv.dtype), _p(recv), _p(out_local),
+                         _stream(recv.device)))
+    return out_local
 
 
 def lse_merge(desc: SegDesc, o_part, lse_part, out, lse):

@@ -265,6 +265,8 @@ std::vector<int64_t> plan_key(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dt
   return k;
 }
 
+zl_status insert_plan(Plan&& p, hipStream_t stream, Plan** out);
+
 // Returns the cached plan for this descriptor, building and uploading it on a
 // miss.  Caller holds g_mu.
 zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int op, hipStream_t stream,
@@ -309,6 +311,12 @@ zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int
     p.host.resize(items.size() * sizeof(zl::Item));
     if (!items.empty()) std::memcpy(p.host.data(), items.data(), p.host.size());
   }
+  return insert_plan(std::move(p), stream, out);
+}
+
+// Uploads a built plan and caches it (most recent first, evicting the oldest
+// beyond kMaxPlans).  Caller holds g_mu.
+zl_status insert_plan(Plan&& p, hipStream_t stream, Plan** out) {
   if (!p.host.empty()) {
     if (hipMalloc(&p.dev, p.host.size()) != hipSuccess)
       return fail(ZL_ERR_HIP, "hipMalloc of a %zu-byte work table failed", p.host.size());
@@ -331,6 +339,77 @@ zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int
     g_plans.pop_back();
   }
   *out = &g_plans.front();
+  return ZL_OK;
+}
+
+// ------------------------------------------------------------- Ulysses row map
+
+// Row map of a Ulysses group: rank-major row (rank j's rows, then j+1's, each
+// in sequence order) -> row of the full-sequence layout.  cu_rank[j*(n+1)+s]
+// is where sequence s starts among rank j's local rows.  Caller holds g_mu.
+zl_status get_rowmap(int32_t group, int32_t nseq, const int32_t* cu_rank, hipStream_t stream, Plan** out,
+                     int64_t* total_rows) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(ZL_ERR_HIP, "hipGetDevice failed: no usable GPU");
+  std::vector<int64_t> key = {100, dev, group, nseq};
+  for (int64_t i = 0; i < (int64_t)group * (nseq + 1); ++i) key.push_back(cu_rank[i]);
+  const int64_t w = nseq + 1;
+  int64_t total = 0;
+  for (int32_t j = 0; j < group; ++j) total += cu_rank[j * w + nseq];
+  *total_rows = total;
+  for (auto it = g_plans.begin(); it != g_plans.end(); ++it) {
+    if (it->key == key) {
+      g_plans.splice(g_plans.begin(), g_plans, it);
+      *out = &g_plans.front();
+      return ZL_OK;
+    }
+  }
+  // full-layout start of each sequence and of each rank's shard inside it
+  std::vector<int64_t> seq_start(nseq + 1, 0);
+  for (int32_t s = 0; s < nseq; ++s) {
+    int64_t len = 0;
+    for (int32_t j = 0; j < group; ++j) len += cu_rank[j * w + s + 1] - cu_rank[j * w + s];
+    seq_start[s + 1] = seq_start[s] + len;
+  }
+  Plan p;
+  p.key = std::move(key);
+  p.device = dev;
+  p.host.resize((size_t)total * sizeof(int32_t));
+  int32_t* map = reinterpret_cast<int32_t*>(p.host.data());
+  std::vector<int64_t> before(nseq, 0);  // rows of sequence s on ranks < j
+  int64_t r = 0;
+  for (int32_t j = 0; j < group; ++j) {
+    for (int32_t s = 0; s < nseq; ++s) {
+      const int32_t n = cu_rank[j * w + s + 1] - cu_rank[j * w + s];
+      for (int32_t o = 0; o < n; ++o) map[r++] = (int32_t)(seq_start[s] + before[s] + o);
+      before[s] += n;
+    }
+  }
+  return insert_plan(std::move(p), stream, out);
+}
+
+zl_status validate_ulysses(int32_t group, int32_t H, int32_t hd, zl_dtype dt) {
+  if (group < 1) return fail(ZL_ERR_INVALID_ARG, "group must be >= 1 (got %d)", group);
+  if (H < 1 || H % group != 0)
+    return fail(ZL_ERR_INVALID_ARG, "num_heads %d must be a positive multiple of the group size %d", H, group);
+  if (hd != 64 && hd != 128) return fail(ZL_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", hd);
+  if (dt != ZL_BF16) return fail(ZL_ERR_UNSUPPORTED, "Ulysses staging is bf16 only");
+  return ZL_OK;
+}
+
+zl_status validate_cu_rank(int32_t group, int32_t nseq, const int32_t* cu_rank, int64_t* total_rows) {
+  if (nseq < 0) return fail(ZL_ERR_INVALID_ARG, "negative sequence count");
+  if (!cu_rank) return fail(ZL_ERR_INVALID_ARG, "cu_rank is NULL");
+  int64_t total = 0;
+  for (int32_t j = 0; j < group; ++j) {
+    const int32_t* c = cu_rank + (int64_t)j * (nseq + 1);
+    if (c[0] != 0) return fail(ZL_ERR_INVALID_ARG, "cu_rank of rank %d must start at 0", j);
+    for (int32_t s = 0; s < nseq; ++s)
+      if (c[s + 1] < c[s]) return fail(ZL_ERR_INVALID_ARG, "cu_rank of rank %d decreases at sequence %d", j, s);
+    total += c[nseq];
+  }
+  if (total >= ((int64_t)1 << 31)) return fail(ZL_ERR_UNSUPPORTED, "more than 2^31-1 rows");
+  *total_rows = total;
   return ZL_OK;
 }
 
@@ -495,6 +574,97 @@ zl_status zl_attn_fwd_step(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dt
     return dt == ZL_BF16 ? zl::launch_fwd_bf16(p, hd, s) : zl::launch_fwd_fp32(p, hd, s);
   });
   return hip_status(e, "ring-step forward launch");
+}
+
+zl_status zl_ulysses_pack_qkv(int32_t group, int32_t t_local, int32_t H, int32_t hd, zl_dtype dt, const void* q,
+                              const void* k, const void* v, void* send, void* stream) {
+  zl_status st = validate_ulysses(group, H, hd, dt);
+  if (st != ZL_OK) return st;
+  if (t_local < 0) return fail(ZL_ERR_INVALID_ARG, "negative t_local");
+  if (t_local == 0) return ok();
+  if (!q || !k || !v || !send) return fail(ZL_ERR_INVALID_ARG, "q, k, v and send must not be NULL");
+  for (const void* p : {q, k, v, (const void*)send})
+    if (!aligned(p, 16)) return fail(ZL_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  zl::UlyssesParams p{};
+  p.a = q;
+  p.b = k;
+  p.c = v;
+  p.dst = send;
+  p.rows = t_local;
+  p.heads = H;
+  p.heads_local = H / group;
+  p.group = group;
+  return hip_status(zl::launch_ulysses(p, 0, hd, static_cast<hipStream_t>(stream)), "Ulysses pack_qkv launch");
+}
+
+zl_status zl_ulysses_unpack_qkv(int32_t group, int32_t num_seqs, const int32_t* cu_rank, int32_t H, int32_t hd,
+                                zl_dtype dt, const void* recv, void* q, void* k, void* v, void* stream) {
+  zl_status st = validate_ulysses(group, H, hd, dt);
+  if (st != ZL_OK) return st;
+  int64_t total = 0;
+  if ((st = validate_cu_rank(group, num_seqs, cu_rank, &total)) != ZL_OK) return st;
+  if (total == 0) return ok();
+  if (!recv || !q || !k || !v) return fail(ZL_ERR_INVALID_ARG, "recv, q, k and v must not be NULL");
+  for (const void* p : {recv, (const void*)q, (const void*)k, (const void*)v})
+    if (!aligned(p, 16)) return fail(ZL_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  std::lock_guard<std::mutex> lock(g_mu);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Plan* plan = nullptr;
+  if ((st = get_rowmap(group, num_seqs, cu_rank, s, &plan, &total)) != ZL_OK) return st;
+  zl::UlyssesParams p{};
+  p.a = recv;
+  p.dst = q;
+  p.dst2 = k;
+  p.dst3 = v;
+  p.row_map = static_cast<const int32_t*>(plan->dev);
+  p.rows = total;
+  p.heads = H;
+  p.heads_local = H / group;
+  p.group = group;
+  return hip_status(zl::launch_ulysses(p, 1, hd, s), "Ulysses unpack_qkv launch");
+}
+
+zl_status zl_ulysses_pack_out(int32_t group, int32_t num_seqs, const int32_t* cu_rank, int32_t H, int32_t hd,
+                              zl_dtype dt, const void* out, void* send, void* stream) {
+  zl_status st = validate_ulysses(group, H, hd, dt);
+  if (st != ZL_OK) return st;
+  int64_t total = 0;
+  if ((st = validate_cu_rank(group, num_seqs, cu_rank, &total)) != ZL_OK) return st;
+  if (total == 0) return ok();
+  if (!out || !send) return fail(ZL_ERR_INVALID_ARG, "out and send must not be NULL");
+  if (!aligned(out, 16) || !aligned(send, 16)) return fail(ZL_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  std::lock_guard<std::mutex> lock(g_mu);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Plan* plan = nullptr;
+  if ((st = get_rowmap(group, num_seqs, cu_rank, s, &plan, &total)) != ZL_OK) return st;
+  zl::UlyssesParams p{};
+  p.a = out;
+  p.dst = send;
+  p.row_map = static_cast<const int32_t*>(plan->dev);
+  p.rows = total;
+  p.heads = H;
+  p.heads_local = H / group;
+  p.group = group;
+  return hip_status(zl::launch_ulysses(p, 2, hd, s), "Ulysses pack_out launch");
+}
+
+zl_status zl_ulysses_unpack_out(int32_t group, int32_t t_local, int32_t H, int32_t hd, zl_dtype dt, const void* recv,
+                                void* out_local, void* stream) {
+  zl_status st = validate_ulysses(group, H, hd, dt);
+  if (st != ZL_OK) return st;
+  if (t_local < 0) return fail(ZL_ERR_INVALID_ARG, "negative t_local");
+  if (t_local == 0) return ok();
+  if (!recv || !out_local) return fail(ZL_ERR_INVALID_ARG, "recv and out_local must not be NULL");
+  if (!aligned(recv, 16) || !aligned(out_local, 16))
+    return fail(ZL_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  zl::UlyssesParams p{};
+  p.a = recv;
+  p.dst = out_local;
+  p.rows = t_local;
+  p.heads = H;
+  p.heads_local = H / group;
+  p.group = group;
+  return hip_status(zl::launch_ulysses(p, 3, hd, static_cast<hipStream_t>(stream)), "Ulysses unpack_out launch");
 }
 
 zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype out_dt, const float* o_part,

@@ -112,7 +112,24 @@ struct BwdParams {
 
 hipError_t launch_fwd_bf16(const FwdParams& p, int head_dim, hipStream_t s);
 hipError_t launch_fwd_fp32(const FwdParams& p, int head_dim, hipStream_t s);
+// Ulysses staging (layout kernels around the head-subset attention); op 0
+// pack_qkv, 1 unpack_qkv, 2 pack_out, 3 unpack_out.
+struct UlyssesParams {
+  const void* a;              // source (q for pack_qkv)
+  const void* b;              // k (pack_qkv)
+  const void* c;              // v (pack_qkv)
+  void* dst;                  // destination (q for unpack_qkv)
+  void* dst2;                 // k (unpack_qkv)
+  void* dst3;                 // v (unpack_qkv)
+  const int32_t* row_map;     // rank-major row -> full row (unpack_qkv, pack_out)
+  int64_t rows;               // local rows (ops 0, 3) or rank-major = full rows (ops 1, 2)
+  int32_t heads;              // H of the local layout
+  int32_t heads_local;        // H / group
+  int32_t group;
+};
+
 hipError_t launch_merge(const MergeParams& p, int head_dim, bool out_bf16, hipStream_t s);
+hipError_t launch_ulysses(const UlyssesParams& p, int op, int head_dim, hipStream_t s);
 // stage 0: preprocess (D), 1: dK/dV, 2: dQ
 hipError_t launch_bwd_bf16(const BwdParams& p, int head_dim, int stage, hipStream_t s);
 

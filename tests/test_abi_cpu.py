@@ -16,7 +16,8 @@ def test_exports_every_declared_symbol():
     names = api.header_symbols()
     assert {"zl_attn_fwd", "zl_attn_bwd", "zl_lse_merge", "zl_plan_dump", "zl_workspace_size",
             "zl_last_error", "zl_abi_version", "zl_shutdown", "zl_profile_enable", "zl_profile_read",
-            "zl_profile_reset", "zl_attn_fwd_step"} <= set(names)
+            "zl_profile_reset", "zl_attn_fwd_step", "zl_ulysses_pack_qkv", "zl_ulysses_unpack_qkv",
+            "zl_ulysses_pack_out", "zl_ulysses_unpack_out"} <= set(names)
     for n in names:
         assert hasattr(api._lib, n), n
 
@@ -132,3 +133,31 @@ def test_ring_step_rules():
     # misaligned accumulator
     assert _step(_step_desc(), flags=0, ptrs=(FAKE,) * 5 + (FAKE + 4, FAKE)) == api.ZL_ERR_INVALID_ARG
     assert "16-byte" in api.last_error()
+
+
+def test_ulysses_rules():
+    q = FAKE
+    # group must divide the heads, bf16 only, head_dim 64/128
+    assert api._u_pack_qkv(3, 8, 8, 128, api.ZL_BF16, q, q, q, q, None) == api.ZL_ERR_INVALID_ARG
+    assert "multiple" in api.last_error()
+    assert api._u_pack_qkv(0, 8, 8, 128, api.ZL_BF16, q, q, q, q, None) == api.ZL_ERR_INVALID_ARG
+    assert api._u_pack_qkv(2, 8, 8, 128, api.ZL_FP32, q, q, q, q, None) == api.ZL_ERR_UNSUPPORTED
+    assert api._u_pack_qkv(2, 8, 8, 96, api.ZL_BF16, q, q, q, q, None) == api.ZL_ERR_UNSUPPORTED
+    assert api._u_pack_qkv(2, 8, 8, 128, api.ZL_BF16, q, None, q, q, None) == api.ZL_ERR_INVALID_ARG
+    assert api._u_unpack_out(2, 8, 8, 128, api.ZL_BF16, q + 8, q, None) == api.ZL_ERR_INVALID_ARG
+    assert "16-byte" in api.last_error()
+    # cu_rank rules
+    bad = np.array([[0, 3, 2], [0, 1, 4]], np.int32)
+    assert api._u_unpack_qkv(2, 2, bad.ctypes.data_as(api._i32p), 8, 128, api.ZL_BF16, q, q, q, q,
+                             None) == api.ZL_ERR_INVALID_ARG and "decreases" in api.last_error()
+    bad = np.array([[1, 3, 4], [0, 1, 4]], np.int32)
+    assert api._u_pack_out(2, 2, bad.ctypes.data_as(api._i32p), 8, 128, api.ZL_BF16, q, q,
+                           None) == api.ZL_ERR_INVALID_ARG and "start at 0" in api.last_error()
+    good = np.array([[0, 3, 4], [0, 1, 4]], np.int32)
+    assert api._u_pack_out(2, 2, good.ctypes.data_as(api._i32p), 8, 128, api.ZL_BF16, None, q,
+                           None) == api.ZL_ERR_INVALID_ARG
+    # empty work is a no-op that needs no device
+    assert api._u_pack_qkv(2, 0, 8, 128, api.ZL_BF16, None, None, None, None, None) == api.ZL_OK
+    empty = np.zeros((2, 3), np.int32)
+    assert api._u_unpack_qkv(2, 2, empty.ctypes.data_as(api._i32p), 8, 128, api.ZL_BF16, None, None, None, None,
+                             None) == api.ZL_OK
