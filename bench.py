@@ -36,11 +36,15 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c4", help="c2..c5 (default c4: coalesced whole+shard)")
-    ap.add_argument("--mode", default="blocks", choices=("blocks", "ring", "gather"),
+    ap.add_argument("--ulysses-group", type=int, default=8, help="group size h for --mode ulysses")
+    ap.add_argument("--mode", default="blocks", choices=("blocks", "ring", "gather", "ulysses"),
                     help="how a shard's K/V blocks reach the forward: blocks = all blocks in one launch plus "
                          "the LSE merge (default); ring = one ring step per block with the merge fused into "
                          "the epilogue (fillers spread over the steps); gather = one launch against the "
-                         "concatenated blocks (all-gather), no partials and no merge")
+                         "concatenated blocks (all-gather), no partials and no merge; ulysses = one GPU's "
+                         "share of the batch's WHOLE sequences under Ulysses (1,h,1): QKV pack, unpack, "
+                         "attention on H/h heads over the full sequences, output pack and unpack (the two "
+                         "all-to-alls are RCCL's and not run here: the send buffer stands in for the receive)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="accumulate oracle heads until this much CPU time is spent")
@@ -237,7 +241,48 @@ def main():
             api.lse_merge(desc, o_part, lse_part, out, lse)
         api.attn_bwd(desc, q, k, v, out, lse, do, w.scale, dq, dk, dv, ws)
 
-    if args.mode == "gather":
+    if args.mode == "ulysses":
+        G = args.ulysses_group
+        assert all(kd == W.WHOLE for kd in w.kind) and H % G == 0, "ulysses mode: a WHOLE-only batch, H % h == 0"
+        Hl = H // G
+        lens = [int(w.cu_seqlens_q[s + 1] - w.cu_seqlens_q[s]) for s in range(w.num_segments)]
+        # even shards (the first ones one longer where a length does not divide)
+        shard = [[n // G + (1 if j < n % G else 0) for n in lens] for j in range(G)]
+        import numpy as np
+        cu_rank = np.array([np.concatenate([[0], np.cumsum(sh)]) for sh in shard], np.int32)
+        t_local = int(cu_rank[0][-1])
+        t_full = w.total_q
+        ql, kl, vl = q[:t_local], k[:t_local], v[:t_local]      # this rank's local rows (any rows of the right shape)
+        send_qkv = torch.empty((G, t_local, Hl, 3, hd), dtype=q.dtype, device=dev)
+        recv_qkv = torch.empty((t_full, Hl, 3, hd), dtype=q.dtype, device=dev)
+        qf, kf_, vf = (torch.empty((t_full, Hl, hd), dtype=q.dtype, device=dev) for _ in range(3))
+        of = torch.empty((t_full, Hl, hd), dtype=q.dtype, device=dev)
+        lf = torch.empty((t_full, Hl), dtype=torch.float32, device=dev)
+        dof = do[:, :Hl].contiguous()
+        dqf, dkf, dvf = (torch.empty((t_full, Hl, hd), dtype=q.dtype, device=dev) for _ in range(3))
+        send_o = torch.empty((t_full, Hl, hd), dtype=q.dtype, device=dev)
+        recv_o = torch.empty((G, t_local, Hl, hd), dtype=q.dtype, device=dev)
+        out_local = torch.empty((t_local, H, hd), dtype=q.dtype, device=dev)
+        ws_u = torch.empty(api.workspace_size(desc, Hl, hd, q.dtype, api.ZL_OP_BWD), dtype=torch.uint8, device=dev)
+        # the all-to-alls are not on this GPU: the receive buffers are filled once from a real pack
+        # (a rank-major permutation of actual rows) and keep their content between the calls
+        api.ulysses_pack_qkv(G, ql, kl, vl, send_qkv)
+        recv_qkv.view(-1).copy_(send_qkv.view(-1))
+        api.ulysses_pack_out(G, cu_rank, qf.copy_(q[:, :Hl]), H, send_o)
+        recv_o.view(-1).copy_(send_o.view(-1))
+        H_report = Hl
+
+        def step():
+            api.ulysses_pack_qkv(G, ql, kl, vl, send_qkv)
+            api.ulysses_unpack_qkv(G, cu_rank, recv_qkv, H, qf, kf_, vf)
+            api.attn_fwd(desc, qf, kf_, vf, w.scale, of, lf, None, None)
+            api.attn_bwd(desc, qf, kf_, vf, of, lf, dof, w.scale, dqf, dkf, dvf, ws_u)
+            api.ulysses_pack_out(G, cu_rank, of, H, send_o)
+            api.ulysses_unpack_out(G, recv_o, H, out_local)
+        ulysses_bytes = {
+            "pack_qkv": 2 * 3 * t_local * H * hd * 2, "unpack_qkv": 2 * 3 * t_full * Hl * hd * 2,
+            "pack_out": 2 * t_full * Hl * hd * 2, "unpack_out": 2 * t_local * H * hd * 2}
+    elif args.mode == "gather":
         gdesc = api.SegDesc.of(gathered_descriptor(w))
 
         def step():
@@ -282,6 +327,8 @@ def main():
     avg = {name: (t / args.steps if n else 0.0) for name, (t, n) in kt.items()}
 
     pairs = w.pair_count()
+    if args.mode == "ulysses":
+        H = H_report            # this GPU computes H/h heads of every sequence
     fa_flops = 14.0 * hd * H * pairs
     value = fa_flops / (ms * 1e-3) / 1e12
     # MFMA FLOPs each kernel executes per block-diagonal pair (x d x H):
@@ -320,6 +367,16 @@ def main():
         gbs = mbytes / (avg["merge"] * 1e-3) / 1e9
         rec["merge_kernel"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": mbytes}
+    if args.mode == "ulysses":
+        total_b = sum(ulysses_bytes.values())
+        ums = avg.get("ulysses", 0.0)
+        rec["config"]["ulysses_group"] = args.ulysses_group
+        rec["config"]["heads_per_gpu"] = H
+        rec["ulysses_staging"] = {"bound": "hbm", "ms": round(ums, 4), "bytes": total_b,
+                                  "achieved": round(total_b / (ums * 1e-3) / 1e9, 1) if ums else None,
+                                  "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                  "frac": round(total_b / (ums * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if ums else None,
+                                  "bytes_per_call": ulysses_bytes}
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(rec), flush=True)

@@ -262,9 +262,18 @@ zl_status zl_plan_dump(const zl_seg_desc* desc, int32_t num_heads, int32_t head_
  * stream it is launched on.  zl_profile_read waits for the pending events of
  * one kernel family, adds their elapsed times to its totals and returns the
  * totals since the last reset.  Kernel ids: ZL_K_FWD, ZL_K_MERGE,
- * ZL_K_BWD_PRE, ZL_K_BWD_DKDV, ZL_K_BWD_DQ.
+ * ZL_K_BWD_PRE, ZL_K_BWD_DKDV, ZL_K_BWD_DQ, ZL_K_ULYSSES (the four Ulysses
+ * staging calls together).
  */
-enum { ZL_K_FWD = 0, ZL_K_MERGE = 1, ZL_K_BWD_PRE = 2, ZL_K_BWD_DKDV = 3, ZL_K_BWD_DQ = 4, ZL_K_COUNT = 5 };
+enum {
+  ZL_K_FWD = 0,
+  ZL_K_MERGE = 1,
+  ZL_K_BWD_PRE = 2,
+  ZL_K_BWD_DKDV = 3,
+  ZL_K_BWD_DQ = 4,
+  ZL_K_ULYSSES = 5,
+  ZL_K_COUNT = 6
+};
 zl_status zl_profile_enable(int32_t on);
 zl_status zl_profile_read(int32_t kernel_id, double* total_ms, int64_t* launches);
 void zl_profile_reset(void);

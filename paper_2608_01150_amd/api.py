@@ -97,9 +97,9 @@ _prof_read = _sig("zl_profile_read", ctypes.c_int, ctypes.c_int32, ctypes.POINTE
                   ctypes.POINTER(ctypes.c_int64))
 _prof_reset = _sig("zl_profile_reset", None)
 
-ZL_K_FWD, ZL_K_MERGE, ZL_K_BWD_PRE, ZL_K_BWD_DKDV, ZL_K_BWD_DQ = range(5)
+ZL_K_FWD, ZL_K_MERGE, ZL_K_BWD_PRE, ZL_K_BWD_DKDV, ZL_K_BWD_DQ, ZL_K_ULYSSES = range(6)
 KERNEL_NAMES = {ZL_K_FWD: "fwd", ZL_K_MERGE: "merge", ZL_K_BWD_PRE: "bwd_pre", ZL_K_BWD_DKDV: "bwd_dkdv",
-                ZL_K_BWD_DQ: "bwd_dq"}
+                ZL_K_BWD_DQ: "bwd_dq", ZL_K_ULYSSES: "ulysses"}
 
 
 def profile_enable(on: bool) -> None:

@@ -594,7 +594,8 @@ zl_status zl_ulysses_pack_qkv(int32_t group, int32_t t_local, int32_t H, int32_t
   p.heads = H;
   p.heads_local = H / group;
   p.group = group;
-  return hip_status(zl::launch_ulysses(p, 0, hd, static_cast<hipStream_t>(stream)), "Ulysses pack_qkv launch");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return hip_status(timed(ZL_K_ULYSSES, s, [&] { return zl::launch_ulysses(p, 0, hd, s); }), "Ulysses pack_qkv launch");
 }
 
 zl_status zl_ulysses_unpack_qkv(int32_t group, int32_t num_seqs, const int32_t* cu_rank, int32_t H, int32_t hd,
@@ -621,7 +622,7 @@ zl_status zl_ulysses_unpack_qkv(int32_t group, int32_t num_seqs, const int32_t* 
   p.heads = H;
   p.heads_local = H / group;
   p.group = group;
-  return hip_status(zl::launch_ulysses(p, 1, hd, s), "Ulysses unpack_qkv launch");
+  return hip_status(timed(ZL_K_ULYSSES, s, [&] { return zl::launch_ulysses(p, 1, hd, s); }), "Ulysses unpack_qkv launch");
 }
 
 zl_status zl_ulysses_pack_out(int32_t group, int32_t num_seqs, const int32_t* cu_rank, int32_t H, int32_t hd,
@@ -645,7 +646,7 @@ zl_status zl_ulysses_pack_out(int32_t group, int32_t num_seqs, const int32_t* cu
   p.heads = H;
   p.heads_local = H / group;
   p.group = group;
-  return hip_status(zl::launch_ulysses(p, 2, hd, s), "Ulysses pack_out launch");
+  return hip_status(timed(ZL_K_ULYSSES, s, [&] { return zl::launch_ulysses(p, 2, hd, s); }), "Ulysses pack_out launch");
 }
 
 zl_status zl_ulysses_unpack_out(int32_t group, int32_t t_local, int32_t H, int32_t hd, zl_dtype dt, const void* recv,
@@ -664,7 +665,8 @@ zl_status zl_ulysses_unpack_out(int32_t group, int32_t t_local, int32_t H, int32
   p.heads = H;
   p.heads_local = H / group;
   p.group = group;
-  return hip_status(zl::launch_ulysses(p, 3, hd, static_cast<hipStream_t>(stream)), "Ulysses unpack_out launch");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return hip_status(timed(ZL_K_ULYSSES, s, [&] { return zl::launch_ulysses(p, 3, hd, s); }), "Ulysses unpack_out launch");
 }
 
 zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype out_dt, const float* o_part,
