@@ -15,10 +15,14 @@ Modules
              per segment and over a packed whole+shard batch.
   routing    which packed rows go where (segment, kind, global position,
              partial slot) and the canonical set of query-tile work items.
+  planner    Filler Packing (Sec. IV-C, Eq. 8): the greedy that places whole
+             fillers into the compute and memory headroom the anchors leave.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against things other
 than itself: 50-digit ``decimal`` brute force, closed forms, finite
-differences, and the invariants the paper's exactness claims imply.  No
+differences, the invariants the paper's exactness claims imply, and for the
+planner the textbook greedy rules it reduces to (LPT, worst fit) and Graham's
+LPT bound against brute-force optima.  No
 function here is "parity unpinned".
 """
 from .attention import (  # noqa: F401
@@ -30,3 +34,4 @@ from .attention import (  # noqa: F401
     segment_rows,
 )
 from .routing import row_routing, work_items  # noqa: F401
+from .planner import filler_pack, load_floor  # noqa: F401
