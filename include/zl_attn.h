@@ -51,7 +51,8 @@ typedef enum {
   ZL_ERR_INVALID_ARG = 1, /* malformed descriptor, pointer, size or scale */
   ZL_ERR_UNSUPPORTED = 2, /* valid request this build does not implement  */
   ZL_ERR_WORKSPACE = 3,   /* workspace missing or too small               */
-  ZL_ERR_HIP = 4          /* the HIP runtime reported an error            */
+  ZL_ERR_HIP = 4,         /* the HIP runtime reported an error            */
+  ZL_ERR_INFEASIBLE = 5   /* a planner found no feasible placement        */
 } zl_status;
 
 /* Segment kinds (Sec. IV-A: (1,1,1) keeps a sequence whole; a split
@@ -255,6 +256,36 @@ zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t num_heads, int32_t head_d
 zl_status zl_plan_dump(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
                        int32_t op, int32_t* items, size_t cap, size_t* n,
                        int32_t* tile_m, int32_t* tile_n);
+
+/*
+ * Filler Packing, Stage 2 of the two-stage planner (Sec. IV-C, Eq. 8).  Host
+ * only: no device work, callable without a GPU.  Fillers stay whole and are
+ * placed one at a time in decreasing price (equal prices keep their input
+ * order).  With compute headroom h^C_r = F - C_r and memory headroom
+ * h^M_r = M_cap - M_r, filler s may go to rank r when h^M_r >= M_{s,r}; it goes
+ * to the feasible rank with the largest min((h^C_r - p_s) / F,
+ * (h^M_r - M_{s,r}) / M_cap), the lowest rank on a tie, and that rank's
+ * ledgers grow by p_s and M_{s,r}.  All arithmetic is IEEE double in exactly
+ * that order, so the decisions are reproducible.
+ *
+ *   num_ranks    N >= 1;  num_fillers n >= 0
+ *   price        [n]      p_s: the filler's profiled whole-sequence price (>= 0)
+ *   mem          [n][N]   M_{s,whole,r}, row-major (>= 0)
+ *   load_floor   F > 0: every batch sequence's whole price summed, over N
+ *   mem_cap      M_cap > 0
+ *   load         [N] in: C_r after anchor placement; out: plus the fillers placed
+ *   mem_used     [N] in: M_r after anchor placement; out: likewise
+ *   rank_of      [n] out: the rank of each filler, -1 if not placed
+ *   failed       out (may be NULL): the first filler that fit on no rank, or -1
+ * All arrays are caller-owned host memory; every value must be finite.
+ * Returns ZL_OK when every filler is placed, ZL_ERR_INFEASIBLE when one fits
+ * nowhere (planning fails; the outputs hold what was placed before it), and
+ * ZL_ERR_INVALID_ARG (nothing written) for NULL arrays, negative or non-
+ * finite values, or a non-positive F or M_cap.
+ */
+zl_status zl_fill_pack(int32_t num_ranks, int32_t num_fillers, const double* price, const double* mem,
+                       double load_floor, double mem_cap, double* load, double* mem_used, int32_t* rank_of,
+                       int32_t* failed);
 
 /*
  * Per-kernel timing with HIP events (off by default).  While enabled, every

@@ -17,7 +17,7 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libzl_attn.so")
 
-ZL_OK, ZL_ERR_INVALID_ARG, ZL_ERR_UNSUPPORTED, ZL_ERR_WORKSPACE, ZL_ERR_HIP = range(5)
+ZL_OK, ZL_ERR_INVALID_ARG, ZL_ERR_UNSUPPORTED, ZL_ERR_WORKSPACE, ZL_ERR_HIP, ZL_ERR_INFEASIBLE = range(6)
 ZL_WHOLE, ZL_SHARD = 0, 1
 ZL_BF16, ZL_FP32 = 0, 1
 ZL_OP_FWD, ZL_OP_BWD, ZL_OP_BWD_DQ = 0, 1, 2
@@ -91,6 +91,9 @@ _bwd = _sig("zl_attn_bwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ct
             _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_uint32, _vp, ctypes.c_size_t, _vp)
 _plan_dump = _sig("zl_plan_dump", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_int32,
                   _i32p, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t), _i32p, _i32p)
+_f64p = ctypes.POINTER(ctypes.c_double)
+_fill_pack = _sig("zl_fill_pack", ctypes.c_int, ctypes.c_int32, ctypes.c_int32, _f64p, _f64p, ctypes.c_double,
+                  ctypes.c_double, _f64p, _f64p, _i32p, ctypes.POINTER(ctypes.c_int32))
 _shutdown = _sig("zl_shutdown", None)
 _prof_enable = _sig("zl_profile_enable", ctypes.c_int, ctypes.c_int32)
 _prof_read = _sig("zl_profile_read", ctypes.c_int, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
@@ -216,6 +219,30 @@ def plan_dump(desc: SegDesc, num_heads: int, head_dim: int, dtype: torch.dtype, 
         _check(_plan_dump(desc.ptr(), num_heads, head_dim, _dtype_code(dtype), op, items.ctypes.data_as(_i32p),
                           items.shape[0], ctypes.byref(n), None, None))
     return items, (tm.value, tn.value)
+
+
+def fill_pack(price, mem, load, mem_used, load_floor: float, mem_cap: float):
+    """zl_fill_pack (Filler Packing, Eq. 8) on host arrays.
+
+    price [n], mem [n, N], load [N] and mem_used [N] (the ledgers after anchor
+    placement).  Returns (rank_of int32 [n], load [N], mem_used [N], failed),
+    failed = index of the first filler that fit nowhere, or None.  Raises
+    ZlError for invalid arguments.
+    """
+    price = np.ascontiguousarray(price, dtype=np.float64)
+    n = price.shape[0]
+    ld = np.array(load, dtype=np.float64)
+    mu = np.array(mem_used, dtype=np.float64)
+    N = ld.shape[0]
+    mem = np.ascontiguousarray(np.asarray(mem, dtype=np.float64).reshape(n, N))
+    rank_of = np.full(n, -1, dtype=np.int32)
+    failed = ctypes.c_int32(-1)
+    st = _fill_pack(N, n, price.ctypes.data_as(_f64p), mem.ctypes.data_as(_f64p), float(load_floor), float(mem_cap),
+                    ld.ctypes.data_as(_f64p), mu.ctypes.data_as(_f64p), rank_of.ctypes.data_as(_i32p),
+                    ctypes.byref(failed))
+    if st not in (ZL_OK, ZL_ERR_INFEASIBLE):
+        _check(st)
+    return rank_of, ld, mu, (None if failed.value < 0 else int(failed.value))
 
 
 def attn_fwd(desc: SegDesc, q, k, v, scale: float, out=None, lse=None, o_part=None, lse_part=None):

@@ -46,6 +46,17 @@ zl_status ok() {
   return ZL_OK;
 }
 
+}  // namespace
+
+namespace zl {
+zl_status host_status(zl_status st, const char* msg) {
+  if (st == ZL_OK) return ok();
+  return fail(st, "%s", msg);
+}
+}  // namespace zl
+
+namespace {
+
 // Which buffers a validated descriptor touches.
 struct Shape {
   int64_t total_q = 0, total_k = 0;

@@ -7,7 +7,13 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include "zl_attn.h"
+
 namespace zl {
+
+// Records `msg` as the calling thread's zl_last_error (clears it for ZL_OK)
+// and returns st: the one error channel of every C ABI entry point.
+zl_status host_status(zl_status st, const char* msg);
 
 // One unit of work of a launch.  Forward: query rows [q_start, q_start+q_len)
 // of one head against the keys [k_start, k_start+k_len) of one K/V range.

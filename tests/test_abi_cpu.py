@@ -17,7 +17,7 @@ def test_exports_every_declared_symbol():
     assert {"zl_attn_fwd", "zl_attn_bwd", "zl_lse_merge", "zl_plan_dump", "zl_workspace_size",
             "zl_last_error", "zl_abi_version", "zl_shutdown", "zl_profile_enable", "zl_profile_read",
             "zl_profile_reset", "zl_attn_fwd_step", "zl_ulysses_pack_qkv", "zl_ulysses_unpack_qkv",
-            "zl_ulysses_pack_out", "zl_ulysses_unpack_out"} <= set(names)
+            "zl_ulysses_pack_out", "zl_ulysses_unpack_out", "zl_fill_pack"} <= set(names)
     for n in names:
         assert hasattr(api._lib, n), n
 
