@@ -276,6 +276,71 @@ def long_video_shard() -> Workload:
     return dataclasses.replace(w, name="long-shard31110x16+12fill-h40", seed=20260005)
 
 
+# -- bucket catalog and synthetic batches (for the price table) -----------------
+# Wan2.1 latent geometry: 8x spatial VAE compression with 2x2 patches gives
+# (H/16) x (W/16) tokens per latent frame; 4x temporal compression of a
+# 16 fps clip of F = 16*seconds + 1 frames gives 1 + (F-1)/4 latent frames.
+# Frame sizes: 256p = 256x448, 480p = 480x832, 720p = 720x1280, 1080p =
+# 1088x1920 (the height padded to a multiple of 16, which reproduces the
+# 497,760 tokens of a 15 s 1080p video in Sec. I).
+_FRAME = {"256p": (256, 448), "480p": (480, 832), "720p": (720, 1280), "1080p": (1088, 1920)}
+
+
+def tokens_per_frame(res: str) -> int:
+    h, w = _FRAME[res]
+    return (h // 16) * (w // 16)
+
+
+def latent_frames(seconds: int, fps: int = 16) -> int:
+    return 1 + (fps * seconds) // 4
+
+
+def _catalog():
+    cat = {f"img{r[:-1]}": tokens_per_frame(r) for r in _FRAME}
+    for sec in (5, 10, 15):
+        for r in ("480p", "720p", "1080p"):
+            cat[f"vid{r[:-1]}-{sec}s"] = latent_frames(sec) * tokens_per_frame(r)
+    return cat
+
+
+CATALOG = _catalog()       # bucket name -> whole-sequence tokens
+IMAGE_BUCKETS = tuple(b for b in CATALOG if b.startswith("img"))
+
+
+def synthetic_batch(num_ranks: int, tokens_per_rank: int, video_share: float, seconds: int, seed: int):
+    """A seeded mixed image-video batch in the shape of the paper's suites
+    (Sec. V-A: 480p-1080p videos of one duration, 256p-1080p images, a
+    per-GPU token budget and a video-token share).  Videos of uniformly drawn
+    resolution are added while the video tokens stay within the share (at
+    least one video), then images of uniformly drawn resolution until the
+    budget is reached.  Returns bucket names, videos first."""
+    import random
+    rng = random.Random(seed)
+    total = num_ranks * tokens_per_rank
+    vids = [f"vid{r}-{seconds}s" for r in ("480", "720", "1080")]
+    out, vt = [], 0
+    while True:
+        b = rng.choice(vids)
+        if out and vt + CATALOG[b] > video_share * total:
+            break
+        out.append(b)
+        vt += CATALOG[b]
+    t = vt
+    while True:
+        b = rng.choice(IMAGE_BUCKETS)
+        if t + CATALOG[b] > total:
+            break
+        out.append(b)
+        t += CATALOG[b]
+    return out
+
+
+def build_segments(name: str, H: int, d: int, segments, seed: int) -> Workload:
+    """A bf16 fwd+bwd workload from a segment list: ("whole", L, q_offset) or
+    ("shard", Lq, q_offset, [(Lk, k_offset, block), ...])."""
+    return _build(name, H, d, "bf16", segments, seed)
+
+
 WORKLOADS = {
     "c1": tiny_plumbing,
     "c2": image_only,
