@@ -117,8 +117,10 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
   const uint32_t row_bytes = (uint32_t)rs * 2u, stat_bytes = (uint32_t)H * 4u;
   Dma dma;
   dma.init(kw, lane, row_bytes);
-  auto fetch = [&](int t) {
-    const int q0 = t * BQ, nq = it.q_len - q0, b = t % NBUF;
+  // Tile t goes to buffer b = t % NBUF; callers pass b as a literal so that
+  // every LDS address below folds to a per-lane base plus an immediate.
+  auto fetch = [&](int t, int b) __attribute__((always_inline)) {
+    const int q0 = t * BQ, nq = it.q_len - q0;
     if (producer) {
       dma.issue(qs[b], qg + (int64_t)q0 * rs, nq, row_bytes);
       const bool even = (kw & 1) == 0;
@@ -130,7 +132,7 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
     }
   };
 
-  fetch(0);
+  fetch(0, 0);
 
   if (producer) {
     // ---------------------------------------------------------- producer
@@ -152,14 +154,13 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
     // 32*(k%2) + 16*(i/8) + 8g + i%8 of tile k/2, lane = key.
     f32x16 sc[2], dp[2];
     // A(k) interleaved with B(k-1) (has_b); the A operand j is the Q (even j)
-    // or dO (odd j) chunk j/2 of the sub-block's 32 rows.
-    auto phase = [&](int k, bool has_b, int xb) {
-      const int ka = k & 1;
-      const int b = (k >> 1) % NBUF;
+    // or dO (odd j) chunk j/2 of the sub-block's 32 rows.  Sub-block k is half
+    // ka = k % 2 of the tile in buffer b; B(k-1) is half sbb of the tile in
+    // buffer bb (all literals at the call sites).
+    auto phase = [&](int ka, int b, int sbb, int bb, bool has_b, int xb) __attribute__((always_inline)) {
       const char* qa = qs[b] + a_off + 32 * ka * PITCH;
       const char* oa = dos[b] + a_off + 32 * ka * PITCH;
       auto a_op = [&](int j) { return *reinterpret_cast<const u32x4*>(((j & 1) ? oa : qa) + poff<D>(0, (j >> 1) * 16)); };
-      const int kb = max(k - 1, 0), sbb = kb & 1, bb = (kb >> 1) % NBUF;  // B's sub-block and tile buffer
       f32x4 lsv[2][2], dsv[2][2];
       u32x4 pp[2], pds[2];
       u32x4 ring[PFA];
@@ -219,17 +220,23 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
     };
     // Phase 0: A(0).  Phases 2t+1, 2t+2: A(2t+1)+B(2t), A(2t+2)+B(2t+1) (the
     // last A reads an all-zero tile past the end and is never used).  Phase
-    // 2n+1: the consumer's last sub-block.
-    fetch(1);
-    phase(0, false, 0);
-    __syncthreads();
-    for (int t = 0; t < nsteps; ++t) {
-      phase(2 * t + 1, true, 0);
+    // 2n+1: the consumer's last sub-block.  The tile loop is unrolled by
+    // NBUF, r = t % NBUF.
+    auto tile = [&](int t, int r) __attribute__((always_inline)) {
+      phase(1, r, 0, r, true, 0);
       wait_vmem();  // own loads of tile t+1 landed
       __syncthreads();
-      fetch(t + 2);
-      phase(2 * t + 2, true, 1);
+      fetch(t + 2, (r + 2) % NBUF);
+      phase(0, (r + 1) % NBUF, 1, r, true, 1);
       __syncthreads();
+    };
+    fetch(1, 1);
+    phase(0, 0, 0, 0, false, 0);
+    __syncthreads();
+    for (int t = 0; t < nsteps; t += NBUF) {
+      tile(t, 0);
+      if (t + 1 < nsteps) tile(t + 1, 1);
+      if (t + 2 < nsteps) tile(t + 2, 2);
     }
     __syncthreads();
     wait_vmem();  // the lookahead loads must land before the workgroup's LDS is released
@@ -256,8 +263,8 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
   // Operand j -> h = j / (D/32), db = j % (D/32): rows of dO^T (dV) or Q^T
   // (dK); A row m <-> d = db*32 + perm32(m), k <-> queries 16h + 8g ...
   constexpr int NOP = 2 * (D / 32);
-  auto phaseC = [&](int t, int sb, int xb) {
-    const char* tbuf = (is_dk ? qs[t % NBUF] : dos[t % NBUF]) + t_off;
+  auto phaseC = [&](int r, int sb, int xb) __attribute__((always_inline)) {
+    const char* tbuf = (is_dk ? qs[r] : dos[r]) + t_off;
     auto c_op = [&](int j) { return tr_operand<D>(tbuf, sb * 32 + 16 * (j / (D / 32)), (j % (D / 32)) * 32); };
     u32x4 w[2][2];  // [key group][h]
 #pragma unroll
@@ -278,22 +285,27 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
     }
   };
   // Phases 0, 1: nothing to consume yet.  Phases 2t+2, 2t+3: C(2t), C(2t+1).
-  fetch(1);
-  __syncthreads();
-  wait_vmem();  // own loads of tile 1 landed
-  __syncthreads();
-  for (int t = 0; t < nsteps; ++t) {
-    fetch(t + 2);
-    phaseC(t, 0, 0);
+  auto tileC = [&](int t, int r) __attribute__((always_inline)) {
+    fetch(t + 2, (r + 2) % NBUF);
+    phaseC(r, 0, 0);
     __syncthreads();
-    phaseC(t, 1, 1);
+    phaseC(r, 1, 1);
     wait_vmem();  // own loads of tile t+2 landed
     __syncthreads();
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db) asm volatile("" : "+a"(acc[k2][db]));
+      for (int db = 0; db < D / 32; ++db) asm volatile("" : "+v"(acc[k2][db]));
     }
+  };
+  fetch(1, 1);
+  __syncthreads();
+  wait_vmem();  // own loads of tile 1 landed
+  __syncthreads();
+  for (int t = 0; t < nsteps; t += NBUF) {
+    tileC(t, 0);
+    if (t + 1 < nsteps) tileC(t + 1, 1);
+    if (t + 2 < nsteps) tileC(t + 2, 2);
   }
 
   // dK = scale * dK^T or dV = dV^T: register i <-> d = db*32 + 16*(i/8) + 8g + i%8,
