@@ -379,7 +379,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
   const uint32_t a_off = poff<D>(perm32(ln), g * 8);
   const uint32_t t_off = tr_lane_off<D>(lane);
 
-  // Rows past the segment's keys read zero; the step masks those keys.
+  // Rows past the segment's keys read zero (the buffer range check).
   const uint16_t* kg = static_cast<const uint16_t*>(p.k) + ((int64_t)it.k_start * H + it.head) * D;
   const uint16_t* vg = static_cast<const uint16_t*>(p.v) + ((int64_t)it.k_start * H + it.head) * D;
   const bool loads_k = wave < 4;
@@ -395,7 +395,6 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
     const char* ka = kbuf + a_off;
     const char* va = vbuf + a_off;
     const char* kt_ = kbuf + t_off;
-    const int nvalid = it.k_len - kt;
     // S^T and dP^T for keys [kb*32, kb*32+32): D row m <-> key kb*32 + perm32(m).
     u32x4 pds[2][2];
 #pragma unroll
@@ -406,15 +405,16 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
         s = mfma32(*reinterpret_cast<const u32x4*>(ka + poff<D>(kb * 32, kk * 16)), qf[kk], s);
         dp = mfma32(*reinterpret_cast<const u32x4*>(va + poff<D>(kb * 32, kk * 16)), of[kk], dp);
       }
-      // register i <-> key kb*32 + 16*(i/8) + 8g + i%8 of this tile, query = lane's row
+      // register i <-> key kb*32 + 16*(i/8) + 8g + i%8 of this tile, query = lane's row.
+      // P is clamped to [0, 1] (exact: every true P is at most 1), a free
+      // modifier of the exp.  That keeps dS finite for the keys past the
+      // segment, whose K and V rows read as zero (S = 0, so P = 2^-lse2 could
+      // overflow): their dS then multiplies a zero K row and adds exactly
+      // nothing to dQ, so no per-key mask is needed.
       float e[16];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) e[i] = fast_exp2(fmaf(s[i], p.scale_log2, -lse2)) * (dp[i] - dd);
-      if (nvalid < BN) {  // partial last tile: keys past the segment contribute nothing
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          if (kb * 32 + 16 * (i >> 3) + 8 * g + (i & 7) >= nvalid) e[i] = 0.f;
-      }
+      for (int i = 0; i < 16; ++i)
+        e[i] = __builtin_amdgcn_fmed3f(fast_exp2(fmaf(s[i], p.scale_log2, -lse2)), 0.f, 1.f) * (dp[i] - dd);
 #pragma unroll
       for (int i = 0; i < 16; i += 2) pds[kb][i >> 3][(i & 7) >> 1] = pack_bf16(e[i], e[i + 1]);
     }
