@@ -391,42 +391,78 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
     dma.issue(loads_k ? kdst : vdst, src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
   };
 
-  auto step = [&](const char* kbuf, const char* vbuf, int kt) {
+  // One 64-key step as two 32-key blocks kb, software-pipelined inside the
+  // wave so that the softmax VALU work runs under MFMAs:
+  //   S/dP MFMAs of kb 0; S/dP MFMAs of kb 1 with the softmax of kb 0;
+  //   dQ MFMAs of kb 0 with the softmax of kb 1; dQ MFMAs of kb 1.
+  // A operands come from LDS through a ring of loads issued PF MFMAs ahead.
+  auto step = [&](const char* kbuf, const char* vbuf) __attribute__((always_inline)) {
     const char* ka = kbuf + a_off;
     const char* va = vbuf + a_off;
     const char* kt_ = kbuf + t_off;
-    // S^T and dP^T for keys [kb*32, kb*32+32): D row m <-> key kb*32 + perm32(m).
+    constexpr int NSD = 2 * (D / 16) * 2;        // S/dP MFMAs per step (both key blocks)
+    constexpr int NQ = 2 * (D / 32) * 2;         // dQ MFMAs per step
+    // S/dP operand j: key block j/(NSD/2), d chunk (j%(NSD/2))/2, K (even j) or V (odd j).
+    auto a_op = [&](int j) {
+      return *reinterpret_cast<const u32x4*>(((j & 1) ? va : ka) +
+                                             poff<D>((j / (NSD / 2)) * 32, ((j % (NSD / 2)) >> 1) * 16));
+    };
+    // dQ operand m: key block m/(NQ/2), d block (m%(NQ/2))/2, 16-key half m%2 (K^T by transpose reads).
+    auto c_op = [&](int m) {
+      return tr_operand<D>(kt_, (m / (NQ / 2)) * 32 + 16 * (m & 1), ((m % (NQ / 2)) >> 1) * 32);
+    };
+    constexpr int PF = 6, PFC = 3;
+    // register i <-> key kb*32 + 16*(i/8) + 8g + i%8 of this tile, query = lane's row.
+    // P is clamped to [0, 1] (exact: every true P is at most 1), a free
+    // modifier of the exp.  That keeps dS finite for the keys past the
+    // segment, whose K and V rows read as zero (S = 0, so P = 2^-lse2 could
+    // overflow): their dS then multiplies a zero K row and adds exactly
+    // nothing to dQ, so no per-key mask is needed.
+    f32x16 sc[2], dpc[2];
     u32x4 pds[2][2];
+    auto softmax2 = [&](int kb, int i) {  // elements i, i+1 of key block kb -> one packed dS word
+      float e[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x16 s = f32x16{}, dp = f32x16{};
+      for (int u = 0; u < 2; ++u)
+        e[u] = __builtin_amdgcn_fmed3f(fast_exp2(fmaf(sc[kb][i + u], p.scale_log2, -lse2)), 0.f, 1.f) *
+               (dpc[kb][i + u] - dd);
+      pds[kb][i >> 3][(i & 7) >> 1] = pack_bf16(e[0], e[1]);
+    };
+    u32x4 ring[PF];
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        s = mfma32(*reinterpret_cast<const u32x4*>(ka + poff<D>(kb * 32, kk * 16)), qf[kk], s);
-        dp = mfma32(*reinterpret_cast<const u32x4*>(va + poff<D>(kb * 32, kk * 16)), of[kk], dp);
-      }
-      // register i <-> key kb*32 + 16*(i/8) + 8g + i%8 of this tile, query = lane's row.
-      // P is clamped to [0, 1] (exact: every true P is at most 1), a free
-      // modifier of the exp.  That keeps dS finite for the keys past the
-      // segment, whose K and V rows read as zero (S = 0, so P = 2^-lse2 could
-      // overflow): their dS then multiplies a zero K row and adds exactly
-      // nothing to dQ, so no per-key mask is needed.
-      float e[16];
+    for (int j = 0; j < PF; ++j) ring[j] = a_op(j);
 #pragma unroll
-      for (int i = 0; i < 16; ++i)
-        e[i] = __builtin_amdgcn_fmed3f(fast_exp2(fmaf(s[i], p.scale_log2, -lse2)), 0.f, 1.f) * (dp[i] - dd);
+    for (int kb = 0; kb < 2; ++kb) sc[kb] = dpc[kb] = f32x16{};
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < 16; i += 2) pds[kb][i >> 3][(i & 7) >> 1] = pack_bf16(e[i], e[i + 1]);
+    for (int j = 0; j < NSD; ++j) {
+      const u32x4 a = ring[j % PF];
+      if (j + PF < NSD) ring[j % PF] = a_op(j + PF);
+      const int kb = j / (NSD / 2), kk = (j % (NSD / 2)) >> 1;
+      if (j & 1)
+        dpc[kb] = mfma32(a, of[kk], dpc[kb]);
+      else
+        sc[kb] = mfma32(a, qf[kk], sc[kb]);
+      // kb 1's MFMAs carry kb 0's softmax: 16 elements over NSD/2 MFMAs.
+      if (j >= NSD / 2 && ((j - NSD / 2) % (NSD / 16)) == NSD / 16 - 1) softmax2(0, 2 * ((j - NSD / 2) / (NSD / 16)));
+      __builtin_amdgcn_sched_barrier(0);
     }
-    // dQ^T[d, q] += sum_key K^T[d, key] dS^T[key, q]; A row m <-> d = db*32 + perm32(m).
+    u32x4 cring[PFC];
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
+    for (int m = 0; m < PFC; ++m) cring[m] = c_op(m);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2)
-          dq[db] = mfma32(tr_operand<D>(kt_, kb * 32 + 16 * s2, db * 32), pds[kb][s2], dq[db]);
+    for (int m = 0; m < NQ; ++m) {
+      const u32x4 a = cring[m % PFC];
+      if (m + PFC < NQ) cring[m % PFC] = c_op(m + PFC);
+      // kb 0's dQ MFMAs carry kb 1's softmax (finished before kb 1's MFMAs).
+      if (m < NQ / 2) {
+        softmax2(1, (16 / (NQ / 2)) * m);
+        if (16 / (NQ / 2) == 4) softmax2(1, (16 / (NQ / 2)) * m + 2);
       }
+      const int kb = m / (NQ / 2), db = (m % (NQ / 2)) >> 1, s2 = m & 1;
+      dq[db] = mfma32(a, pds[kb][s2], dq[db]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
@@ -438,19 +474,19 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 0 complete; buffers 2 no longer read
       fetch(kt + 2 * BN, ks2, vs2);
-      step(ks0, vs0, kt);
+      step(ks0, vs0);
       kt += BN;
       if (kt >= it.k_len) break;
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
       fetch(kt + 2 * BN, ks0, vs0);
-      step(ks1, vs1, kt);
+      step(ks1, vs1);
       kt += BN;
       if (kt >= it.k_len) break;
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 2 complete; buffers 1 no longer read
       fetch(kt + 2 * BN, ks1, vs1);
-      step(ks2, vs2, kt);
+      step(ks2, vs2);
       kt += BN;
       if (kt >= it.k_len) break;
     }
