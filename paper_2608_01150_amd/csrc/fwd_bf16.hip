@@ -87,71 +87,116 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     dma.issue(loads_k ? kdst : vdst, src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
   };
 
-  auto step = [&](const char* kbuf, const char* vbuf, int kt) {
+  // One 64-key step as two 32-key blocks kb, each its own online-softmax
+  // update (max, lazy rescale, exponentials), software-pipelined inside the
+  // wave so that the softmax VALU work runs under MFMAs:
+  //   S of kb 0;  S of kb 1 with the softmax of kb 0;  max/rescale of kb 1;
+  //   PV of kb 0 with the exponentials of kb 1;  PV of kb 1.
+  // A operands come from LDS through rings of loads issued ahead of use.
+  auto step = [&](const char* kbuf, const char* vbuf, int kt) __attribute__((always_inline)) {
     const char* ka = kbuf + a_off;
     const char* vt = vbuf + t_off;
-    // S^T for keys [kb*32, kb*32+32): D row m <-> key kb*32 + perm32(m).
-    f32x16 s[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      s[kb] = f32x16{};
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk)
-        s[kb] = mfma32(*reinterpret_cast<const u32x4*>(ka + poff<D>(kb * 32, kk * 16)), qf[kk], s[kb]);
-    }
-    // s[kb][i] is the raw score of (key kb*32 + 16*(i/8) + 8*g + i%8, query qr).
+    constexpr int NS = 2 * (D / 16);        // S MFMAs per step
+    constexpr int NP = 2 * (D / 32) * 2;    // PV MFMAs per step
+    constexpr int PF = 6, PFC = 3;
+    // S operand j: keys of block j/(NS/2) (rows perm32), d chunk j%(NS/2).
+    auto a_op = [&](int j) {
+      return *reinterpret_cast<const u32x4*>(ka + poff<D>((j / (NS / 2)) * 32, (j % (NS / 2)) * 16));
+    };
+    // PV operand m: key block m/(NP/2), d block (m%(NP/2))/2, 16-key half m%2.
+    auto c_op = [&](int m) {
+      return tr_operand<D>(vt, (m / (NP / 2)) * 32 + 16 * (m & 1), ((m % (NP / 2)) >> 1) * 32);
+    };
     const int nvalid = it.k_len - kt;
-    if (nvalid < BN) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+    // s[kb][i] is the raw score of (key kb*32 + 16*(i/8) + 8*g + i%8, query qr).
+    f32x16 s[2];
+    u32x4 pb[2][2];
+    float lsum = 0.f;
+    // Max of block kb (keys past the range masked on a partial tile) and the
+    // lazy rescale; a rescale after block 0 was exponentiated also rescales
+    // block 0's packed P, which has not yet entered the PV MFMAs.
+    auto block_max = [&](int kb) {
+      if (nvalid < BN) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int key = kb * 32 + 16 * (i >> 3) + 8 * g + (i & 7);
           if (key >= nvalid) s[kb][i] = kNegBig;
         }
       }
-    }
-    float mt = kNegBig;
+      float mt = s[kb][0];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+      for (int i = 1; i < 16; ++i) mt = fmaxf(mt, s[kb][i]);
+      mt = xor32_max(mt) * p.scale_log2;
+      if (__any(mt > m_run + kRescaleSlack)) {
+        const float m_new = fmaxf(m_run, mt);
+        const float alpha = fast_exp2(m_run - m_new);
+        m_run = m_new;
+        l_part *= alpha;
+        lsum *= alpha;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) mt = fmaxf(mt, s[kb][i]);
-    }
-    mt = fmaxf(mt, __shfl_xor(mt, 32)) * p.scale_log2;
-    if (__any(mt > m_run + kRescaleSlack)) {
-      const float m_new = fmaxf(m_run, mt);
-      const float alpha = fast_exp2(m_run - m_new);
-      m_run = m_new;
-      l_part *= alpha;
+        for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
+          for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+        }
+        if (kb == 1) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+          for (int h = 0; h < 2; ++h) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+              pb[0][h][t] = pack_bf16(bf16_lo(pb[0][h][t]) * alpha, bf16_hi(pb[0][h][t]) * alpha);
+          }
+        }
       }
-    }
-    float lsum = 0.f;
-    u32x4 pb[2][2];
+    };
+    // Exponentials of elements 2c, 2c+1 of block kb: one packed P word.
+    auto expo = [&](int kb, int c) {
+      const float e0 = fast_exp2(fmaf(s[kb][2 * c], p.scale_log2, -m_run));
+      const float e1 = fast_exp2(fmaf(s[kb][2 * c + 1], p.scale_log2, -m_run));
+      lsum += e0 + e1;
+      pb[kb][c >> 2][c & 3] = pack_bf16(e0, e1);
+    };
+
+    u32x4 ring[PF];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int j = 0; j < PF; ++j) ring[j] = a_op(j);
+    s[0] = s[1] = f32x16{};
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < 16; i += 2) {
-        const float e0 = fast_exp2(fmaf(s[kb][i], p.scale_log2, -m_run));
-        const float e1 = fast_exp2(fmaf(s[kb][i + 1], p.scale_log2, -m_run));
-        lsum += e0 + e1;
-        pb[kb][i >> 3][(i & 7) >> 1] = pack_bf16(e0, e1);
+    for (int j = 0; j < NS; ++j) {
+      const u32x4 a = ring[j % PF];
+      if (j + PF < NS) ring[j % PF] = a_op(j + PF);
+      const int kb = j / (NS / 2);
+      s[kb] = mfma32(a, qf[j % (NS / 2)], s[kb]);
+      // Block 1's MFMAs carry block 0's softmax: the max first, then the
+      // eight exponential pairs spread over the remaining slots.
+      if (j == NS / 2) block_max(0);
+      if (j > NS / 2) {
+        constexpr int SLOTS = NS / 2 - 1;
+        const int c0 = (j - NS / 2 - 1) * 8 / SLOTS, c1 = (j - NS / 2) * 8 / SLOTS;
+#pragma unroll
+        for (int c = c0; c < c1; ++c) expo(0, c);
       }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    u32x4 cring[PFC];
+#pragma unroll
+    for (int m = 0; m < PFC; ++m) cring[m] = c_op(m);
+    block_max(1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int m = 0; m < NP; ++m) {
+      const u32x4 a = cring[m % PFC];
+      if (m + PFC < NP) cring[m % PFC] = c_op(m + PFC);
+      // Block 0's PV MFMAs carry block 1's exponentials.
+      if (m < NP / 2) {
+#pragma unroll
+        for (int c = m * 8 / (NP / 2); c < (m + 1) * 8 / (NP / 2); ++c) expo(1, c);
+      }
+      const int kb = m / (NP / 2), db = (m % (NP / 2)) >> 1, s2 = m & 1;
+      o[db] = mfma32(a, pb[kb][s2], o[db]);
+      __builtin_amdgcn_sched_barrier(0);
     }
     l_part += lsum;
-    // O^T[d, q] += sum_key V^T[d, key] P^T[key, q]; A row m <-> d = db*32 + perm32(m).
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2)
-          o[db] = mfma32(tr_operand<D>(vt, kb * 32 + 16 * s2, db * 32), pb[kb][s2], o[db]);
-      }
-    }
   };
 
   // Three buffer sets in rotation, the loop unrolled by three.  Tile t+2 is
@@ -187,7 +232,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
   }
 
   // Epilogue.  o[db][i] is (d = db*32 + 16*(i/8) + 8*g + i%8, query qr).
-  const float l = l_part + __shfl_xor(l_part, 32);
+  const float l = xor32_sum(l_part);
   const float inv = l > 0.f ? 1.f / l : 0.f;
   const float lse = l > 0.f ? (m_run + __log2f(l)) * kLn2 : -INFINITY;
   if (!q_ok) return;

@@ -209,6 +209,19 @@ __device__ __forceinline__ void step_weights(bool first, float lse_acc, float ls
   lse = m + logf(den);
 }
 
+// Max / sum of a value over lanes l and l^32 with v_permlane32_swap (a VALU
+// exchange of the two 32-lane halves, no LDS round trip).  With both operands
+// equal, the swap returns the lower half's values in every lane of the first
+// result and the upper half's in the second.
+__device__ __forceinline__ float xor32_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
