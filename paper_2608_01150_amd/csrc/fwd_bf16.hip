@@ -120,7 +120,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int key = kb * 32 + 16 * (i >> 3) + 8 * g + (i & 7);
-          if (key >= nvalid) s[kb][i] = kNegBig;
+          if (key >= nvalid) s[kb][i] = -INFINITY;  // exact at any positive scale
         }
       }
       float mt = s[kb][0];

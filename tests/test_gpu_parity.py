@@ -60,10 +60,10 @@ def _shard_rows_slots(d):
     return out
 
 
-def run_and_compare(d, H, hd, dtype, seed, backward=True):
+def run_and_compare(d, H, hd, dtype, seed, backward=True, scale=None):
     desc = api.SegDesc.of(d)
     q, k, v, do = _inputs(d, H, hd, dtype, seed)
-    scale = 1.0 / hd ** 0.5
+    scale = 1.0 / hd ** 0.5 if scale is None else scale
     qd, kd_, vd, dod = (t.cuda() for t in (q, k, v, do))
     tq = q.shape[0]
     nan = float("nan")
@@ -162,6 +162,16 @@ def test_edge_lengths_bf16():
                     kv_first=(0, 1, 2, 3, 5), kv_count=(1, 1, 1, 2, 2),
                     cu_k=(0, 1, 64, 193, 194, 257, 322, 450), block_index=(0, 0, 0, 1, 0, 0, 1), num_slots=2)
     run_and_compare(d, 2, 128, torch.bfloat16, 3)
+
+
+def test_tiny_softmax_scale_masks_exactly():
+    """Any finite positive scale is valid; at 1e-30 every score is ~0, so keys
+    past a range must be masked by -inf itself (a large finite negative score
+    would shrink to O(1) after scaling and take softmax weight)."""
+    d = _descs.desc(cu_q=(0, 1, 64, 193, 320, 385), kind=(0, 0, 0, 1, 1),
+                    kv_first=(0, 1, 2, 3, 5), kv_count=(1, 1, 1, 2, 2),
+                    cu_k=(0, 1, 64, 193, 194, 257, 322, 450), block_index=(0, 0, 0, 1, 0, 0, 1), num_slots=2)
+    run_and_compare(d, 2, 128, torch.bfloat16, 5, scale=1e-30)
 
 
 def test_constant_v_returns_that_row():
