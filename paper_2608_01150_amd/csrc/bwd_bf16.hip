@@ -60,8 +60,8 @@ __global__ __launch_bounds__(NT) void bwd_pre_kernel(BwdParams p) {
 // ------------------------------------------------------------------ dK / dV
 // Warp-specialised: a workgroup of 8 waves takes 128 keys, as four key groups
 // of 32.  Producer wave w (0-3) holds key group w; consumer waves 4-7 each
-// hold two key groups' dV or dK accumulators (see the consumer), and every
-// SIMD runs one producer and one consumer.  The segment's queries are
+// hold the dV or dK accumulators of one half of d for all 128 keys (see the
+// consumer), and every SIMD runs one producer and one consumer.  The segment's queries are
 // processed as 32-query sub-blocks k (two per 64-query tile):
 //   A(k)  producer: S = Q K^T, dP = dO V^T (MFMA, K and V in registers)
 //   B(k)  producer: P = exp(S - LSE), dS = P (dP - D) (VALU), written to LDS
@@ -244,44 +244,45 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
   }
 
   // ------------------------------------------------------------ consumer
-  // Consumer wave 4 + 2*kp + o owns key groups 2kp, 2kp+1 (64 keys) and one
-  // output: dV (o = 0) or dK (o = 1).  Every transpose-read operand (dO^T or
-  // Q^T) then feeds two MFMAs, one per key group.
-  const int ci = wave - 4, kp = ci >> 1;
-  const bool is_dk = (ci & 1) != 0;
-  f32x16 acc[2][D / 32];
+  // Consumer wave 4 + ci owns one output, dV (ci < 2) or dK (ci >= 2), for
+  // all 128 keys of the item and half of the d rows, dh = ci % 2.  Every
+  // transpose-read operand (dO^T or Q^T rows of its d half) feeds four MFMAs,
+  // one per key group, and the exchange words (P or dS of each key group) are
+  // 16-byte reads: per sub-block 2*NDT operands of two transpose reads and
+  // eight exchange reads for 16 MFMAs (d = 128).
+  const int ci = wave - 4;
+  const bool is_dk = ci >= 2;
+  const int dh = ci & 1;
+  constexpr int NDT = D / 64;                   // 32-row d tiles per consumer
+  f32x16 acc[4][NDT];                           // [key group][d tile]
 #pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) {
+  for (int kg = 0; kg < 4; ++kg) {
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) acc[k2][db] = f32x16{};
+    for (int dt = 0; dt < NDT; ++dt) acc[kg][dt] = f32x16{};
   }
   wait_vmem();  // tile 0 landed (own loads)
   __syncthreads();  // tile 0 published
 
-  constexpr int PFC = 3;
-  // C(k): sub-block k = 2t + sb of tile t, P or dS from exchange buffer xb.
-  // Operand j -> h = j / (D/32), db = j % (D/32): rows of dO^T (dV) or Q^T
-  // (dK); A row m <-> d = db*32 + perm32(m), k <-> queries 16h + 8g ...
-  constexpr int NOP = 2 * (D / 32);
+  // C(k): sub-block k = 2t + sb of tile t (buffer r), P or dS from exchange
+  // buffer xb.  Operand (h, dt): rows d = (dh*NDT + dt)*32 + perm32(m) of dO^T
+  // (dV) or Q^T (dK), k <-> queries 16h + 8g ... of the sub-block.
   auto phaseC = [&](int r, int sb, int xb) __attribute__((always_inline)) {
     const char* tbuf = (is_dk ? qs[r] : dos[r]) + t_off;
-    auto c_op = [&](int j) { return tr_operand<D>(tbuf, sb * 32 + 16 * (j / (D / 32)), (j % (D / 32)) * 32); };
-    u32x4 w[2][2];  // [key group][h]
+    u32x4 a[2][NDT], w[4][2];
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
+    for (int h = 0; h < 2; ++h) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) w[k2][h] = xch[xb][2 * kp + k2][(is_dk ? 2 : 0) + h][lane];
+      for (int dt = 0; dt < NDT; ++dt) a[h][dt] = tr_operand<D>(tbuf, sb * 32 + 16 * h, (dh * NDT + dt) * 32);
+#pragma unroll
+      for (int kg = 0; kg < 4; ++kg) w[kg][h] = xch[xb][kg][(is_dk ? 2 : 0) + h][lane];
     }
-    u32x4 ring[PFC];
 #pragma unroll
-    for (int j = 0; j < PFC; ++j) ring[j] = c_op(j);
+    for (int h = 0; h < 2; ++h) {
 #pragma unroll
-    for (int j = 0; j < NOP; ++j) {
-      const u32x4 a = ring[j % PFC];
-      if (j + PFC < NOP) ring[j % PFC] = c_op(j + PFC);
-      const int h = j / (D / 32), db = j % (D / 32);
-      acc[0][db] = mfma32(a, w[0][h], acc[0][db]);
-      acc[1][db] = mfma32(a, w[1][h], acc[1][db]);
+      for (int dt = 0; dt < NDT; ++dt) {
+#pragma unroll
+        for (int kg = 0; kg < 4; ++kg) acc[kg][dt] = mfma32(a[h][dt], w[kg][h], acc[kg][dt]);
+      }
     }
   };
   // Phases 0, 1: nothing to consume yet.  Phases 2t+2, 2t+3: C(2t), C(2t+1).
@@ -293,9 +294,9 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
     wait_vmem();  // own loads of tile t+2 landed
     __syncthreads();
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
+    for (int kg = 0; kg < 4; ++kg) {
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db) asm volatile("" : "+v"(acc[k2][db]));
+      for (int dt = 0; dt < NDT; ++dt) asm volatile("" : "+v"(acc[kg][dt]));
     }
   };
   fetch(1, 1);
@@ -308,24 +309,24 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
     if (t + 2 < nsteps) tileC(t + 2, 2);
   }
 
-  // dK = scale * dK^T or dV = dV^T: register i <-> d = db*32 + 16*(i/8) + 8g + i%8,
-  // key = key group's lane key.
+  // dK = scale * dK^T or dV = dV^T: register i <-> d = (dh*NDT + dt)*32 +
+  // 16*(i/8) + 8g + i%8, key = key group kg's lane key.
   const float osc = is_dk ? p.scale : 1.f;
   uint16_t* og = static_cast<uint16_t*>(is_dk ? p.dk : p.dv);
 #pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) {
-    const int okey = (2 * kp + k2) * 32 + ln;
+  for (int kg = 0; kg < 4; ++kg) {
+    const int okey = kg * 32 + ln;
     if (okey >= it.k_len) continue;
     uint16_t* dst = og + ((int64_t)(it.k_start + okey) * H + it.head) * D;
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
+    for (int dt = 0; dt < NDT; ++dt) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         u32x4 wo;
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-          wo[t] = pack_bf16(acc[k2][db][8 * h + 2 * t] * osc, acc[k2][db][8 * h + 2 * t + 1] * osc);
-        *reinterpret_cast<u32x4*>(dst + db * 32 + 16 * h + 8 * g) = wo;
+          wo[t] = pack_bf16(acc[kg][dt][8 * h + 2 * t] * osc, acc[kg][dt][8 * h + 2 * t + 1] * osc);
+        *reinterpret_cast<u32x4*>(dst + (dh * NDT + dt) * 32 + 16 * h + 8 * g) = wo;
       }
     }
   }
