@@ -2,7 +2,7 @@
 
 One step = the whole path over one packed batch: one forward launch over the
 WHOLE and SHARD segments together, the LSE merge of the shard partials, and
-the backward (preprocess, main, dQ finalize), inputs resident in HBM.  The
+the backward (preprocess, dK/dV, dQ), inputs resident in HBM.  The
 default workload is the coalesced whole+shard batch: one GPU's share of a
 75,600-token 720p video at CP=8 (a 9450-query shard against all 8 K/V blocks
 of 9450 tokens) packed with six whole 1560-token images, 40 heads, d=128,
@@ -11,7 +11,7 @@ bf16.  It is the one batch that exercises every step of the path.
 Prints one JSON line.  value = fwd+bwd TFLOP/s with the FlashAttention FLOP
 convention (forward 4*d*H*pairs, backward 10*d*H*pairs, pairs = block-diagonal
 query-key pairs only).  roofline = the dominant (longest) kernel, timed with
-HIP events on its own stream inside the timed region and priced at the MFMA
+HIP events on the stream it is launched on inside the timed region and priced at the MFMA
 FLOPs it executes per pair (forward 4d, dK/dV 8d, dQ 6d) against the bf16
 dense MFMA peak.
 cpu_baseline = the fp64 oracle timed on this host's cores on a bounded
