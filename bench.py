@@ -367,6 +367,12 @@ def main():
         gbs = mbytes / (avg["merge"] * 1e-3) / 1e9
         rec["merge_kernel"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": mbytes}
+    # Host scheduler: building the forward, dK/dV and dQ work tables of this batch (what the cached
+    # plan saves on every later call; zl_plan_dump runs the same builder on the host).
+    t0 = time.perf_counter()
+    for op in (api.ZL_OP_FWD, api.ZL_OP_BWD, api.ZL_OP_BWD_DQ):
+        api.plan_dump(desc, H, hd, q.dtype, op)
+    rec["host_scheduler_ms"] = round((time.perf_counter() - t0) * 1e3, 3)
     if args.mode == "ulysses":
         total_b = sum(ulysses_bytes.values())
         ums = avg.get("ulysses", 0.0)
