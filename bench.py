@@ -40,7 +40,8 @@ def parse():
     ap.add_argument("--mode", default="blocks", choices=("blocks", "ring", "gather", "ulysses"),
                     help="how a shard's K/V blocks reach the forward: blocks = all blocks in one launch plus "
                          "the LSE merge (default); ring = one ring step per block with the merge fused into "
-                         "the epilogue (fillers spread over the steps); gather = one launch against the "
+                         "the epilogue (fillers spread over the steps) and one backward step per block with "
+                         "dQ accumulated across the steps (fillers in the last); gather = one launch against the "
                          "concatenated blocks (all-gather), no partials and no merge; ulysses = one GPU's "
                          "share of the batch's WHOLE sequences under Ulysses (1,h,1): QKV pack, unpack, "
                          "attention on H/h heads over the full sequences, output pack and unpack (the two "
@@ -159,6 +160,38 @@ def ring_steps(w, q, k, v):
                         lse=torch.empty((qr.shape[0], q.shape[1]), dtype=torch.float32, device=q.device),
                         n_shard_rows=n_sq))
     return out
+
+
+def ring_bwd_steps(w, q, k, v, out, lse, do, dq, dk, dv):
+    """Backward ring steps over the packed batch: step r brings block r of the (single, leading) shard,
+    and the last step also carries every WHOLE filler, whose K/V rows follow the last block.  Every step
+    works on views of the full tensors (the shard's rows are the first rows), so dK/dV and dQ land in
+    place."""
+    import numpy as np
+    from paper_2608_01150_amd import api
+    from paper_2608_01150_amd import workloads as W
+    assert w.kind[0] == W.SHARD and all(kd == W.WHOLE for kd in w.kind[1:]), "ring backward: one leading shard"
+    R = w.kv_count[0]
+    n_sq = int(w.cu_seqlens_q[1])
+    cu_k = [int(x) for x in w.cu_seqlens_k]
+    steps = []
+    for r in range(R):
+        last = r == R - 1
+        nseg = w.num_segments if last else 1
+        rows = w.total_q if last else n_sq
+        b0 = cu_k[w.kv_first[0] + r]
+        k_end = w.total_k if last else cu_k[w.kv_first[0] + r + 1]
+        lk = [cu_k[w.kv_first[0] + r + 1] - b0] + [cu_k[w.kv_first[s] + 1] - cu_k[w.kv_first[s]]
+                                                    for s in range(1, nseg)]
+        desc = api.SegDesc(np.asarray(w.cu_seqlens_q[:nseg + 1], np.int32),
+                           np.asarray(w.kind[:nseg], np.uint8), np.arange(nseg, dtype=np.int32),
+                           np.ones(nseg, np.int32), np.concatenate([[0], np.cumsum(lk)]).astype(np.int32),
+                           np.zeros(nseg, np.int32), 1)
+        sl, ks = slice(0, rows), slice(b0, k_end)
+        steps.append(dict(desc=desc, q=q[sl], out=out[sl], lse=lse[sl], do=do[sl], dq=dq[sl], k=k[ks], v=v[ks],
+                          dk=dk[ks], dv=dv[ks],
+                          flags=(api.ZL_STEP_FIRST if r == 0 else 0) | (api.ZL_STEP_LAST if last else 0)))
+    return steps
 
 
 # Source files whose text determines each kernel's code; a stored counter
@@ -300,13 +333,17 @@ def main():
         if w.num_slots:
             api.lse_merge(desc, o_part, lse_part, out, lse)
         R = len(steps_in)
+        bsteps = ring_bwd_steps(w, q, k, v, out, lse, do, dq, dk, dv)
+        dq_acc = torch.empty((n_sq, H, hd), dtype=torch.float32, device=dev)
 
         def step():
             for r, st in enumerate(steps_in):
                 flags = (api.ZL_STEP_FIRST if r == 0 else 0) | (api.ZL_STEP_LAST if r == R - 1 else 0)
                 api.attn_fwd_step(st["desc"], st["q"], st["k"], st["v"], w.scale, st["out"], st["lse"], o_acc,
                                   lse_acc, flags)
-            api.attn_bwd(desc, q, k, v, out, lse, do, w.scale, dq, dk, dv, ws)
+            for b in bsteps:
+                api.attn_bwd_step(b["desc"], b["q"], b["k"], b["v"], b["out"], b["lse"], b["do"], w.scale, b["dq"],
+                                  b["dk"], b["dv"], dq_acc, b["flags"], ws)
 
     for _ in range(args.warmup):
         step()

@@ -238,6 +238,31 @@ zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t num_heads, int32_t head_d
                       void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Backward of one ring step (Sec. II-B ring attention, Tab. II (1,1,k); the
+ * counterpart of zl_attn_fwd_step).  Every SHARD segment brings exactly one
+ * K/V block (kv_count == 1; block_index may be NULL); out and lse are the
+ * FINAL (merged) outputs of its rows.  The call writes that block's dK/dV
+ * (this query chunk's contribution, for the block's owner) and folds the
+ * block's dQ sum into the shard rows' running fp32 accumulator:
+ *   flags & ZL_STEP_FIRST:  the accumulator starts from this block;
+ *   flags & ZL_STEP_LAST:   dq (bf16) = scale * (accumulator + this block);
+ *   otherwise the sum goes back to dq_acc and dq is not written for them.
+ * WHOLE segments ride along in any step and are complete in it (dq, dk, dv
+ * written).  FIRST|LAST equals zl_attn_bwd.  dq_acc: [Tq, H, d] fp32 device
+ * memory indexed by packed query row (so a SHARD segment must occupy the
+ * same packed rows in every step), caller-owned, 16-byte aligned; may be NULL
+ * when flags is FIRST|LAST or no row is SHARD.  Sums are per row and head in
+ * one workgroup: no atomics, deterministic.  Other arguments, workspace and
+ * errors as zl_attn_bwd, plus ZL_ERR_INVALID_ARG for unknown flags, a SHARD
+ * with kv_count != 1, or a missing dq_acc.
+ */
+zl_status zl_attn_bwd_step(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
+                           float softmax_scale, const void* q, const void* k, const void* v,
+                           const void* out, const float* lse, const void* dout,
+                           void* dq, void* dk, void* dv, float* dq_acc, uint32_t flags,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Host-only view of the schedule a launch would use (no device work): the
  * work items of op in issue order, 8 int32 each:
  *   q_start, q_len, k_start, k_len, head, slot (-1 for WHOLE), segment, range.

@@ -89,6 +89,8 @@ _merge = _sig("zl_lse_merge", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32,
               ctypes.c_int32, _vp, _vp, _vp)
 _bwd = _sig("zl_attn_bwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
             _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_uint32, _vp, ctypes.c_size_t, _vp)
+_bwd_step = _sig("zl_attn_bwd_step", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
+                 _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_uint32, _vp, ctypes.c_size_t, _vp)
 _plan_dump = _sig("zl_plan_dump", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_int32,
                   _i32p, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t), _i32p, _i32p)
 _f64p = ctypes.POINTER(ctypes.c_double)
@@ -338,6 +340,18 @@ def attn_bwd(desc: SegDesc, q, k, v, out, lse, dout, scale: float, dq=None, dk=N
         workspace = torch.empty(workspace_size(desc, h, d, q.dtype, ZL_OP_BWD), dtype=torch.uint8, device=dev)
     _check(_bwd(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
                 _p(dout), _p(dq), _p(dk), _p(dv), 0, _p(workspace), workspace.numel(), _stream(dev)))
+    return dq, dk, dv
+
+
+def attn_bwd_step(desc: SegDesc, q, k, v, out, lse, dout, scale: float, dq, dk, dv, dq_acc, flags: int,
+                  workspace=None):
+    """zl_attn_bwd_step: one ring step of the backward (see the header); returns (dq, dk, dv)."""
+    tq, h, d = q.shape
+    if workspace is None:
+        workspace = torch.empty(workspace_size(desc, h, d, q.dtype, ZL_OP_BWD), dtype=torch.uint8, device=q.device)
+    _check(_bwd_step(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
+                     _p(dout), _p(dq), _p(dk), _p(dv), _p(dq_acc), int(flags), _p(workspace), workspace.numel(),
+                     _stream(q.device)))
     return dq, dk, dv
 
 

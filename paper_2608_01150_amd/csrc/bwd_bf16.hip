@@ -497,15 +497,38 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
   // dq[db][i] is (d = db*32 + 16*(i/8) + 8g + i%8, query qr).
   if (!q_ok) return;
   uint16_t* dqg = static_cast<uint16_t*>(p.dq) + qrow * D;
+  // Ring step, SHARD row: fold this block's sum into the fp32 accumulator;
+  // only the last step writes dQ (one item per row and head: no atomics).
+  const bool accumulate = p.step_mode && it.slot >= 0;
+  float* accg = accumulate ? p.dq_acc + qrow * D : nullptr;
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
+      const int d0 = db * 32 + 16 * h + 8 * g;
+      float v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = dq[db][8 * h + t];
+      if (accumulate) {
+        f32x4* ap = reinterpret_cast<f32x4*>(accg + d0);
+        if (!p.step_first) {
+          const f32x4 a0 = ap[0], a1 = ap[1];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            v[t] += a0[t];
+            v[4 + t] += a1[t];
+          }
+        }
+        if (!p.step_last) {
+          ap[0] = f32x4{v[0], v[1], v[2], v[3]};
+          ap[1] = f32x4{v[4], v[5], v[6], v[7]};
+          continue;
+        }
+      }
       u32x4 w;
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        w[t] = pack_bf16(dq[db][8 * h + 2 * t] * p.scale, dq[db][8 * h + 2 * t + 1] * p.scale);
-      *reinterpret_cast<u32x4*>(dqg + db * 32 + 16 * h + 8 * g) = w;
+      for (int t = 0; t < 4; ++t) w[t] = pack_bf16(v[2 * t] * p.scale, v[2 * t + 1] * p.scale);
+      *reinterpret_cast<u32x4*>(dqg + d0) = w;
     }
   }
 }

@@ -182,7 +182,13 @@ TileCfg tile_cfg(zl_dtype dt, int op) {
   return TileCfg{zl::kBwdTileM, zl::kBwdTileN};
 }
 
-std::vector<zl::Item> build_items(const zl_seg_desc* d, int32_t H, int op, TileCfg t) {
+// Internal plan kinds beside the public ZL_OP_* codes: the merge table, and
+// the backward of a ring step, whose dQ items mark SHARD rows (slot 0).
+constexpr int kPlanMerge = 2;
+constexpr int kPlanBwdStep = 5;
+
+// mark_shard: dQ items of SHARD segments carry slot 0 instead of -1.
+std::vector<zl::Item> build_items(const zl_seg_desc* d, int32_t H, int op, TileCfg t, bool mark_shard = false) {
   std::vector<zl::Item> items;
   for (int32_t s = 0; s < d->num_q_segs; ++s) {
     const int32_t q0 = d->cu_seqlens_q[s], q1 = d->cu_seqlens_q[s + 1];
@@ -194,7 +200,8 @@ std::vector<zl::Item> build_items(const zl_seg_desc* d, int32_t H, int op, TileC
       const int32_t total = d->cu_seqlens_k[j1] - d->cu_seqlens_k[j0];
       for (int32_t h = 0; h < H; ++h)
         for (int32_t t0 = q0; t0 < q1; t0 += t.m)
-          items.push_back({t0, std::min(t.m, q1 - t0), d->cu_seqlens_k[j0], total, h, -1, s, j0});
+          items.push_back({t0, std::min(t.m, q1 - t0), d->cu_seqlens_k[j0], total, h, mark_shard && shard ? 0 : -1, s,
+                           j0});
       continue;
     }
     for (int32_t j = d->kv_first[s]; j < d->kv_first[s] + d->kv_count[s]; ++j) {
@@ -295,7 +302,7 @@ zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int
   Plan p;
   p.key = std::move(key);
   p.device = dev;
-  if (op == 2) {
+  if (op == kPlanMerge) {
     MergeTable t = build_merge(d, H);
     p.n_segs = (int32_t)t.segs.size();
     p.n_units = t.units;
@@ -304,9 +311,9 @@ zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int
     p.host.resize(p.slots_offset + t.slots.size() * sizeof(int32_t));
     if (seg_bytes) std::memcpy(p.host.data(), t.segs.data(), seg_bytes);
     if (!t.slots.empty()) std::memcpy(p.host.data() + p.slots_offset, t.slots.data(), t.slots.size() * 4);
-  } else if (op == ZL_OP_BWD) {
+  } else if (op == ZL_OP_BWD || op == kPlanBwdStep) {
     std::vector<zl::Item> kv = build_items(d, H, ZL_OP_BWD, tile_cfg(dt, ZL_OP_BWD));
-    std::vector<zl::Item> qi = build_items(d, H, ZL_OP_BWD_DQ, tile_cfg(dt, ZL_OP_BWD_DQ));
+    std::vector<zl::Item> qi = build_items(d, H, ZL_OP_BWD_DQ, tile_cfg(dt, ZL_OP_BWD_DQ), op == kPlanBwdStep);
     if (kv.size() > (size_t)INT32_MAX || qi.size() > (size_t)INT32_MAX)
       return fail(ZL_ERR_UNSUPPORTED, "too many work items");
     p.n_items = (int32_t)kv.size();
@@ -694,7 +701,7 @@ zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype 
   std::lock_guard<std::mutex> lock(g_mu);
   Plan* plan = nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = get_plan(desc, H, hd, out_dt, 2, s, &plan)) != ZL_OK) return st;
+  if ((st = get_plan(desc, H, hd, out_dt, kPlanMerge, s, &plan)) != ZL_OK) return st;
   if (plan->n_units == 0) return ok();
   zl::MergeParams p{};
   p.o_part = o_part;
@@ -712,23 +719,35 @@ zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype 
                     "merge launch");
 }
 
-zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
-                      const void* k, const void* v, const void* out, const float* lse, const void* dout, void* dq,
-                      void* dk, void* dv, uint32_t flags, void* workspace, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared by zl_attn_bwd (step = false) and zl_attn_bwd_step.
+zl_status attn_bwd_impl(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
+                        const void* k, const void* v, const void* out, const float* lse, const void* dout, void* dq,
+                        void* dk, void* dv, bool step, float* dq_acc, uint32_t flags, void* workspace,
+                        size_t ws_bytes, void* stream) {
   zl_status st = validate_common(H, hd, dt, scale, true);
   if (st != ZL_OK) return st;
   if (dt != ZL_BF16) return fail(ZL_ERR_UNSUPPORTED, "backward supports ZL_BF16 only");
-  if (flags != 0) return fail(ZL_ERR_INVALID_ARG, "flags must be 0");
+  if (!step && flags != 0) return fail(ZL_ERR_INVALID_ARG, "flags must be 0");
+  if (step && (flags & ~(uint32_t)(ZL_STEP_FIRST | ZL_STEP_LAST)))
+    return fail(ZL_ERR_INVALID_ARG, "flags may only hold ZL_STEP_FIRST and ZL_STEP_LAST");
+  const bool first = !step || (flags & ZL_STEP_FIRST), last = !step || (flags & ZL_STEP_LAST);
   Shape sh;
-  if ((st = validate_desc(desc, 0, false, &sh)) != ZL_OK) return st;
+  if ((st = validate_desc(desc, 0, false, &sh, step)) != ZL_OK) return st;
   if ((st = check_sizes(sh, H, hd, 0)) != ZL_OK) return st;
   if (!sh.ranges_single_owner)
     return fail(ZL_ERR_INVALID_ARG, "backward needs every K/V range used by at most one segment");
   if (sh.total_q > 0 && (!q || !out || !lse || !dout || !dq))
     return fail(ZL_ERR_INVALID_ARG, "q, out, lse, dout and dq must not be NULL");
   if (sh.total_k > 0 && (!k || !v || !dk || !dv)) return fail(ZL_ERR_INVALID_ARG, "k, v, dk and dv must not be NULL");
+  if (step && sh.any_shard_rows && !(first && last) && !dq_acc)
+    return fail(ZL_ERR_INVALID_ARG, "dq_acc is needed unless flags = ZL_STEP_FIRST | ZL_STEP_LAST");
   for (const void* p : {q, k, v, out, dout, (const void*)dq, (const void*)dk, (const void*)dv})
     if (p && !aligned(p, 16)) return fail(ZL_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  if (dq_acc && !aligned(dq_acc, 16)) return fail(ZL_ERR_INVALID_ARG, "dq_acc must be 16-byte aligned");
   if (lse && !aligned(lse, 4)) return fail(ZL_ERR_INVALID_ARG, "lse must be 4-byte aligned");
   size_t need = 0;
   if ((st = zl_workspace_size(desc, H, hd, dt, ZL_OP_BWD, &need)) != ZL_OK) return st;
@@ -739,7 +758,7 @@ zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype d
   std::lock_guard<std::mutex> lock(g_mu);
   Plan* plan = nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = get_plan(desc, H, hd, dt, ZL_OP_BWD, s, &plan)) != ZL_OK) return st;
+  if ((st = get_plan(desc, H, hd, dt, step ? kPlanBwdStep : ZL_OP_BWD, s, &plan)) != ZL_OK) return st;
   zl::BwdParams p{};
   p.q = q;
   p.k = k;
@@ -762,10 +781,33 @@ zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype d
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
   p.xcd_chunk = xcd_chunk();
+  p.step_mode = step && !(first && last) ? 1 : 0;
+  p.step_first = first ? 1 : 0;
+  p.step_last = last ? 1 : 0;
+  p.dq_acc = dq_acc;
   hipError_t e = timed(ZL_K_BWD_PRE, s, [&] { return zl::launch_bwd_bf16(p, hd, 0, s); });
   if (e == hipSuccess) e = timed(ZL_K_BWD_DKDV, s, [&] { return zl::launch_bwd_bf16(p, hd, 1, s); });
   if (e == hipSuccess) e = timed(ZL_K_BWD_DQ, s, [&] { return zl::launch_bwd_bf16(p, hd, 2, s); });
   return hip_status(e, "backward launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
+                      const void* k, const void* v, const void* out, const float* lse, const void* dout, void* dq,
+                      void* dk, void* dv, uint32_t flags, void* workspace, size_t ws_bytes, void* stream) {
+  return attn_bwd_impl(desc, H, hd, dt, scale, q, k, v, out, lse, dout, dq, dk, dv, false, nullptr, flags, workspace,
+                       ws_bytes, stream);
+}
+
+zl_status zl_attn_bwd_step(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
+                           const void* k, const void* v, const void* out, const float* lse, const void* dout, void* dq,
+                           void* dk, void* dv, float* dq_acc, uint32_t flags, void* workspace, size_t ws_bytes,
+                           void* stream) {
+  return attn_bwd_impl(desc, H, hd, dt, scale, q, k, v, out, lse, dout, dq, dk, dv, true, dq_acc, flags, workspace,
+                       ws_bytes, stream);
 }
 
 zl_status zl_plan_dump(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, int32_t op, int32_t* items,

@@ -114,6 +114,13 @@ struct BwdParams {
   float scale;
   float scale_log2;
   int32_t xcd_chunk;
+  // Ring-step mode (zl_attn_bwd_step): dQ rows of SHARD items (slot >= 0)
+  // accumulate this call's key block into dq_acc (raw, unscaled sums) and are
+  // written to dq only by the last step.
+  int32_t step_mode;
+  int32_t step_first;    // the accumulator starts from this block
+  int32_t step_last;     // the accumulated dQ (scaled, bf16) goes to dq
+  float* dq_acc;         // [Tq, H, d] fp32
 };
 
 hipError_t launch_fwd_bf16(const FwdParams& p, int head_dim, hipStream_t s);

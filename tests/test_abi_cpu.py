@@ -17,7 +17,7 @@ def test_exports_every_declared_symbol():
     assert {"zl_attn_fwd", "zl_attn_bwd", "zl_lse_merge", "zl_plan_dump", "zl_workspace_size",
             "zl_last_error", "zl_abi_version", "zl_shutdown", "zl_profile_enable", "zl_profile_read",
             "zl_profile_reset", "zl_attn_fwd_step", "zl_ulysses_pack_qkv", "zl_ulysses_unpack_qkv",
-            "zl_ulysses_pack_out", "zl_ulysses_unpack_out", "zl_fill_pack"} <= set(names)
+            "zl_ulysses_pack_out", "zl_ulysses_unpack_out", "zl_fill_pack", "zl_attn_bwd_step"} <= set(names)
     for n in names:
         assert hasattr(api._lib, n), n
 
@@ -133,6 +133,30 @@ def test_ring_step_rules():
     # misaligned accumulator
     assert _step(_step_desc(), flags=0, ptrs=(FAKE,) * 5 + (FAKE + 4, FAKE)) == api.ZL_ERR_INVALID_ARG
     assert "16-byte" in api.last_error()
+
+
+def _bstep(d, flags, acc=FAKE, ptrs=(FAKE,) * 9, dt=api.ZL_BF16):
+    # no workspace: every call below must fail validation before any device work
+    return api._bwd_step(d.ptr(), 2, 64, dt, 0.125, *ptrs, acc, flags, None, 0, None)
+
+
+def test_bwd_step_rules():
+    full = api.ZL_STEP_FIRST | api.ZL_STEP_LAST
+    # a SHARD segment must bring exactly one block per step
+    assert _bstep(_ok_desc(), full) == api.ZL_ERR_INVALID_ARG and "exactly one range" in api.last_error()
+    # unknown flags, bf16 only
+    assert _bstep(_step_desc(), 4) == api.ZL_ERR_INVALID_ARG and "flags" in api.last_error()
+    assert _bstep(_step_desc(), full, dt=api.ZL_FP32) == api.ZL_ERR_UNSUPPORTED
+    # without FIRST|LAST the SHARD rows need the dQ accumulator
+    for flags in (0, api.ZL_STEP_FIRST, api.ZL_STEP_LAST):
+        assert _bstep(_step_desc(), flags, acc=None) == api.ZL_ERR_INVALID_ARG and "dq_acc" in api.last_error()
+    assert _bstep(_step_desc(), 0, acc=FAKE + 4) == api.ZL_ERR_INVALID_ARG and "16-byte" in api.last_error()
+    # otherwise valid: the workspace is checked last
+    assert _bstep(_step_desc(), full, acc=None) == api.ZL_ERR_WORKSPACE
+    assert _bstep(_step_desc(), 0) == api.ZL_ERR_WORKSPACE
+    # the plain backward still rejects any flag
+    assert api._bwd(_step_desc().ptr(), 2, 64, api.ZL_BF16, 0.125, *(FAKE,) * 9, 1, None, 0,
+                    None) == api.ZL_ERR_INVALID_ARG
 
 
 def test_ulysses_rules():

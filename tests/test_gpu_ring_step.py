@@ -143,3 +143,92 @@ def test_all_gather_mode_matches_all_blocks_mode():
     ref = oracle.packed_forward(d, q.double().numpy(), k.double().numpy(), v.double().numpy(), scale)
     np.testing.assert_allclose(to64(out_g), ref["final_out"], rtol=0, atol=O_TOL)
     np.testing.assert_allclose(to64(lse_g), ref["final_lse"], rtol=0, atol=LSE_TOL)
+
+
+def _bwd_tol_check(got, ref, name):
+    got, ref = to64(got), np.asarray(ref)
+    err = np.abs(got - ref).max()
+    assert err <= 2e-2 * max(1.0, np.abs(ref).max()), f"{name}: max abs err {err}"
+    nref = np.linalg.norm(ref)
+    assert nref == 0 or np.linalg.norm(got - ref) / nref <= 2e-2, name
+
+
+@pytest.mark.parametrize("hd,fill_step", [(128, 0), (64, 2), (128, 1)])
+def test_ring_backward_steps_match_all_blocks_backward(hd, fill_step):
+    """zl_attn_bwd_step over a shard's blocks, one per call (FIRST ... LAST),
+    with the WHOLE fillers riding in one step.  Every block's dK/dV and the
+    fillers' dQ/dK/dV are the same work items as in the all-blocks backward
+    and must match it bit for bit; the shard's dQ is summed block by block in
+    fp32 and must match the all-blocks dQ and the oracle to the backward
+    tolerances."""
+    H = 2
+    blocks = (129, 64, 200)          # the shard's K/V blocks, consecutive in K
+    nq, fills = 150, (77, 64, 1)
+    g = torch.Generator().manual_seed(40 + hd + fill_step)
+    R = len(blocks)
+    tq, tk = nq + sum(fills), sum(blocks) + sum(fills)
+    q, do = (torch.randn((tq, H, hd), generator=g).to(torch.bfloat16) for _ in range(2))
+    k, v = (torch.randn((tk, H, hd), generator=g).to(torch.bfloat16) for _ in range(2))
+    scale = 1.0 / hd ** 0.5
+    # all-blocks layout: the shard (rows 0..nq, ranges 0..R-1), then the fillers
+    lq = [nq] + list(fills)
+    cu_q = np.concatenate([[0], np.cumsum(lq)]).astype(np.int32)
+    cu_k = np.concatenate([[0], np.cumsum(list(blocks) + list(fills))]).astype(np.int32)
+    d = dict(cu_seqlens_q=tuple(cu_q), kind=(1,) + (0,) * len(fills),
+             kv_first=(0,) + tuple(R + i for i in range(len(fills))), kv_count=(R,) + (1,) * len(fills),
+             cu_seqlens_k=tuple(cu_k), block_index=tuple(range(R)) + (0,) * len(fills), num_slots=R,
+             q_offset=None, k_offset=None)
+    desc = api.SegDesc.of(d)
+    qd, kd, vd, dod = q.cuda(), k.cuda(), v.cuda(), do.cuda()
+    out, lse, op, lp = api.attn_fwd(desc, qd, kd, vd, scale)
+    api.lse_merge(desc, op, lp, out, lse)
+    dq_ref, dk_ref, dv_ref = api.attn_bwd(desc, qd, kd, vd, out, lse, dod, scale)
+
+    dq = torch.full_like(qd, float("nan"))
+    dq_acc = torch.full((tq, H, hd), float("nan"), device="cuda")
+    nf = len(fills)
+    for r in range(R):
+        with_fill = r == fill_step
+        rows = tq if with_fill else nq
+        b0, b1 = int(cu_k[r]), int(cu_k[r + 1])
+        ks = [kd[b0:b1]] + ([kd[cu_k[R]:]] if with_fill else [])
+        vs = [vd[b0:b1]] + ([vd[cu_k[R]:]] if with_fill else [])
+        kr, vr = torch.cat(ks), torch.cat(vs)
+        lk = [b1 - b0] + (list(fills) if with_fill else [])
+        nseg = 1 + (nf if with_fill else 0)
+        sdesc = api.SegDesc(cu_q[:nseg + 1].copy(), np.array([1] + [0] * (nseg - 1), np.uint8),
+                            np.arange(nseg, dtype=np.int32), np.ones(nseg, np.int32),
+                            np.concatenate([[0], np.cumsum(lk)]).astype(np.int32), np.zeros(nseg, np.int32), 1)
+        dkr = torch.full_like(kr, float("nan"))
+        dvr = torch.full_like(vr, float("nan"))
+        flags = (api.ZL_STEP_FIRST if r == 0 else 0) | (api.ZL_STEP_LAST if r == R - 1 else 0)
+        api.attn_bwd_step(sdesc, qd[:rows], kr, vr, out[:rows], lse[:rows], dod[:rows], scale, dq[:rows], dkr, dvr,
+                          dq_acc, flags)
+        torch.cuda.synchronize()
+        assert torch.equal(dkr[:b1 - b0], dk_ref[b0:b1]) and torch.equal(dvr[:b1 - b0], dv_ref[b0:b1]), r
+        if with_fill:
+            assert torch.equal(dkr[b1 - b0:], dk_ref[cu_k[R]:]) and torch.equal(dvr[b1 - b0:], dv_ref[cu_k[R]:])
+            assert torch.equal(dq[nq:], dq_ref[nq:])
+    _bwd_tol_check(dq[:nq], to64(dq_ref[:nq]), "ring dq vs all-blocks dq")
+    rq, _, _ = oracle.packed_backward(d, q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                      do.double().numpy(), scale)
+    _bwd_tol_check(dq, rq, "ring dq vs oracle")
+
+
+def test_single_backward_step_equals_backward():
+    """flags = FIRST|LAST (no accumulator) is the ordinary backward, bit for bit."""
+    H, hd = 2, 128
+    d = dict(cu_seqlens_q=(0, 97, 161), kind=(1, 0), kv_first=(0, 1), kv_count=(1, 1),
+             cu_seqlens_k=(0, 257, 321), block_index=(0, 0), num_slots=1, q_offset=None, k_offset=None)
+    g = torch.Generator().manual_seed(44)
+    q, do = (torch.randn((161, H, hd), generator=g).to(torch.bfloat16).cuda() for _ in range(2))
+    k, v = (torch.randn((321, H, hd), generator=g).to(torch.bfloat16).cuda() for _ in range(2))
+    desc = api.SegDesc.of(d)
+    scale = hd ** -0.5
+    out, lse, op, lp = api.attn_fwd(desc, q, k, v, scale)
+    api.lse_merge(desc, op, lp, out, lse)
+    dq_ref, dk_ref, dv_ref = api.attn_bwd(desc, q, k, v, out, lse, do, scale)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    api.attn_bwd_step(desc, q, k, v, out, lse, do, scale, dq, dk, dv, None, api.ZL_STEP_FIRST | api.ZL_STEP_LAST)
+    torch.cuda.synchronize()
+    assert torch.equal(dq, dq_ref) and torch.equal(dk, dk_ref) and torch.equal(dv, dv_ref)
