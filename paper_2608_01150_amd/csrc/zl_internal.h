@@ -26,11 +26,11 @@ static_assert(sizeof(Item) == 32, "work item must stay 32 bytes");
 
 // Tile shapes of each kernel family (rows of Q per forward item, keys per
 // backward item, and the inner tile of the loop each one runs).
-constexpr int kFwdTileM = 256;       // bf16 forward: 4 waves x 64 query rows
+constexpr int kFwdTileM = 256;       // bf16 forward: 8 waves x 32 query rows
 constexpr int kFwdTileN = 64;        // keys per inner step
 constexpr int kFwd32TileM = 64;      // fp32 forward: one query row per lane
 constexpr int kFwd32TileN = 32;
-constexpr int kBwdTileN = 128;       // dK/dV kernel: 4 waves x 32 keys per item
+constexpr int kBwdTileN = 128;       // dK/dV kernel: 4 producer waves x 32 keys per item
 constexpr int kBwdTileM = 64;        // queries per dK/dV inner step
 constexpr int kDqTileM = 256;        // dQ kernel: 8 waves x 32 query rows per item
 constexpr int kDqTileN = 64;         // keys per dQ inner step
