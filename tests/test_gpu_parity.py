@@ -234,3 +234,14 @@ def test_ring_step_mode_equals_all_blocks_mode():
         api.attn_fwd(api.SegDesc.of(dj), qd, kd_, vd, 0.09, None, None, o_step, l_step)
     torch.cuda.synchronize()
     assert torch.equal(o_all, o_step) and torch.equal(l_all, l_step)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_descriptors_larger_bf16(seed):
+    """Larger random packed batches (up to 1100 rows per segment or block,
+    several tiles and ragged tails everywhere), both head dims, more heads."""
+    rng = np.random.default_rng(500 + seed)
+    d = _descs.random_desc(rng, 4, 2, 1100, 5)
+    if not d["kind"] or d["cu_seqlens_q"][-1] == 0:
+        pytest.skip("empty draw")
+    run_and_compare(d, 3, (64, 128)[seed % 2], torch.bfloat16, 600 + seed)

@@ -232,3 +232,19 @@ def test_single_backward_step_equals_backward():
     api.attn_bwd_step(desc, q, k, v, out, lse, do, scale, dq, dk, dv, None, api.ZL_STEP_FIRST | api.ZL_STEP_LAST)
     torch.cuda.synchronize()
     assert torch.equal(dq, dq_ref) and torch.equal(dk, dk_ref) and torch.equal(dv, dv_ref)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_ring_steps_random_bf16(seed):
+    """Random ring shapes: 1-2 shards of up to 700 queries, 2-5 blocks of up
+    to 700 keys (some empty), 0-4 fillers in random steps, both head dims."""
+    rng = np.random.default_rng(700 + seed)
+    R = int(rng.integers(2, 6))
+    nsh = int(rng.integers(1, 3))
+    shard_q = tuple(int(rng.integers(1, 701)) for _ in range(nsh))
+    shard_blocks = tuple(tuple(int(rng.integers(0, 701)) for _ in range(R)) for _ in range(nsh))
+    nf = int(rng.integers(0, 5))
+    fillers = tuple(int(rng.integers(1, 701)) for _ in range(nf))
+    fill_step = tuple(int(rng.integers(0, R)) for _ in range(nf))
+    _ring(shard_q, shard_blocks, fillers, fill_step, H=2, hd=(64, 128)[seed % 2], dtype=torch.bfloat16,
+          seed=800 + seed)
