@@ -232,7 +232,7 @@ def stored_traffic(kernel: str, workload: str):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: this build measures one GPU's share of the batch "
+        print("bench.py runs on one GPU only: it measures one GPU's share of the batch "
               "(context parallelism is simulated by feeding that GPU's K/V blocks locally); "
               "--gpus must be 1.", file=sys.stderr)
         sys.exit(2)

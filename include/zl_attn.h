@@ -49,7 +49,7 @@ extern "C" {
 typedef enum {
   ZL_OK = 0,
   ZL_ERR_INVALID_ARG = 1, /* malformed descriptor, pointer, size or scale */
-  ZL_ERR_UNSUPPORTED = 2, /* valid request this build does not implement  */
+  ZL_ERR_UNSUPPORTED = 2, /* valid request the library does not implement */
   ZL_ERR_WORKSPACE = 3,   /* workspace missing or too small               */
   ZL_ERR_HIP = 4,         /* the HIP runtime reported an error            */
   ZL_ERR_INFEASIBLE = 5   /* a planner found no feasible placement        */
