@@ -168,13 +168,19 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       const int kb = j / (NS / 2);
       s[kb] = mfma32(a, qf[j % (NS / 2)], s[kb]);
       // Block 1's MFMAs carry block 0's softmax: the max first, then the
-      // eight exponential pairs spread over the remaining slots.
+      // eight exponential pairs spread over the remaining slots.  Each packed
+      // word and the running sum are pinned where they are computed: block
+      // 1's partial-tile mask is a branch, and without the pin the compiler
+      // sinks this work past it, next to its first use, out of the MFMAs.
       if (j == NS / 2) block_max(0);
       if (j > NS / 2) {
         constexpr int SLOTS = NS / 2 - 1;
         const int c0 = (j - NS / 2 - 1) * 8 / SLOTS, c1 = (j - NS / 2) * 8 / SLOTS;
 #pragma unroll
-        for (int c = c0; c < c1; ++c) expo(0, c);
+        for (int c = c0; c < c1; ++c) {
+          expo(0, c);
+          asm volatile("" : "+v"(pb[0][c >> 2][c & 3]), "+v"(lsum));
+        }
       }
       __builtin_amdgcn_sched_barrier(0);
     }
