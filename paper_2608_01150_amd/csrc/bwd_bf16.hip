@@ -338,7 +338,8 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
 // of K and V, and dQ sums over all of them against the final LSE, so the item
 // streams the segment's keys [k_start, k_start + k_len) as one range: block
 // boundaries play no part in the backward.  64-key K/V tiles rotate through
-// three LDS buffers, fetched two steps ahead (waves 0-3 load K, 4-7 load V).
+// three LDS buffers, fetched two steps ahead (waves 0-3 load K, 4-7 load V,
+// each fetch's instructions spread over a step's S/dP MFMAs).
 constexpr int kDqThreads = 512;
 
 template <int D>
@@ -391,6 +392,14 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
   auto fetch = [&](int kt, char* kdst, char* vdst) {
     dma.issue(loads_k ? kdst : vdst, src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
   };
+  // Inside the loop a fetch is only set up here; the next step's S/dP MFMAs
+  // issue its instructions one at a time (as in the forward kernel).
+  i32x4 next_rsrc;
+  uint32_t next_lds;
+  auto fetch_spread = [&](int kt, char* kdst, char* vdst) {
+    next_rsrc = Dma::resource(src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
+    next_lds = lds_addr(loads_k ? kdst : vdst);
+  };
 
   // One 64-key step as two 32-key blocks kb, software-pipelined inside the
   // wave so that the softmax VALU work runs under MFMAs:
@@ -413,6 +422,8 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
       return tr_operand<D>(kt_, (m / (NQ / 2)) * 32 + 16 * (m & 1), ((m % (NQ / 2)) >> 1) * 32);
     };
     constexpr int PF = 6, PFC = 3;
+    constexpr int DMA_GAP = NSD / DMA_PER_FETCH;  // S/dP MFMAs between the spread fetch's instructions
+    static_assert(DMA_GAP >= 2 && (DMA_PER_FETCH - 1) * DMA_GAP + 1 < NSD, "spread fetch must fit the S/dP MFMAs");
     // register i <-> key kb*32 + 16*(i/8) + 8g + i%8 of this tile, query = lane's row.
     // P is clamped to [0, 1] (exact: every true P is at most 1), a free
     // modifier of the exp.  That keeps dS finite for the keys past the
@@ -444,6 +455,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
         dpc[kb] = mfma32(a, of[kk], dpc[kb]);
       else
         sc[kb] = mfma32(a, qf[kk], sc[kb]);
+      if (j % DMA_GAP == 1 && j / DMA_GAP < DMA_PER_FETCH) dma.issue_one(next_rsrc, next_lds, j / DMA_GAP);
       // kb 1's MFMAs carry kb 0's softmax: 16 elements over NSD/2 MFMAs.
       if (j >= NSD / 2 && ((j - NSD / 2) % (NSD / 16)) == NSD / 16 - 1) softmax2(0, 2 * ((j - NSD / 2) / (NSD / 16)));
       __builtin_amdgcn_sched_barrier(0);
@@ -474,19 +486,19 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
     for (int kt = 0;;) {
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 0 complete; buffers 2 no longer read
-      fetch(kt + 2 * BN, ks2, vs2);
+      fetch_spread(kt + 2 * BN, ks2, vs2);
       step(ks0, vs0);
       kt += BN;
       if (kt >= it.k_len) break;
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
-      fetch(kt + 2 * BN, ks0, vs0);
+      fetch_spread(kt + 2 * BN, ks0, vs0);
       step(ks1, vs1);
       kt += BN;
       if (kt >= it.k_len) break;
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 2 complete; buffers 1 no longer read
-      fetch(kt + 2 * BN, ks1, vs1);
+      fetch_spread(kt + 2 * BN, ks1, vs1);
       step(ks2, vs2);
       kt += BN;
       if (kt >= it.k_len) break;

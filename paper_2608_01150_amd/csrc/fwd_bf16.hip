@@ -13,7 +13,8 @@
 // output is already the B operand of the next MFMA.  K and V tiles are staged
 // row-major (padded pitch, conflict-free) in three LDS buffers by direct
 // global-to-LDS loads issued two steps ahead (waves 0-3 load K, waves 4-7
-// load V), one barrier per step.  A staged tile serves 256 queries, so the
+// load V, each fetch's instructions spread over a step's S MFMAs), one
+// barrier per step.  A staged tile serves 256 queries, so the
 // staging costs half as much per MFMA as with 128-row items.
 //
 // Epilogue: WHOLE items write the final bf16 output and the LSE; SHARD items
@@ -86,6 +87,15 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
   auto fetch = [&](int kt, char* kdst, char* vdst) {
     dma.issue(loads_k ? kdst : vdst, src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
   };
+  // Inside the loop a fetch is only set up here; the next step's S MFMAs
+  // issue its DMA_PER_FETCH instructions one at a time (all of them before
+  // the step ends, so the wait before the next barrier is unchanged).
+  i32x4 next_rsrc;
+  uint32_t next_lds;
+  auto fetch_spread = [&](int kt, char* kdst, char* vdst) {
+    next_rsrc = Dma::resource(src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
+    next_lds = lds_addr(loads_k ? kdst : vdst);
+  };
 
   // One 64-key step as two 32-key blocks kb, each its own online-softmax
   // update (max, lazy rescale, exponentials), software-pipelined inside the
@@ -99,6 +109,8 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     constexpr int NS = 2 * (D / 16);        // S MFMAs per step
     constexpr int NP = 2 * (D / 32) * 2;    // PV MFMAs per step
     constexpr int PF = 6, PFC = 3;
+    constexpr int DMA_GAP = NS / DMA_PER_FETCH;  // S MFMAs between the spread fetch's instructions
+    static_assert(DMA_GAP >= 2 && (DMA_PER_FETCH - 1) * DMA_GAP + 1 < NS, "spread fetch must fit the S MFMAs");
     // S operand j: keys of block j/(NS/2) (rows perm32), d chunk j%(NS/2).
     auto a_op = [&](int j) {
       return *reinterpret_cast<const u32x4*>(ka + poff<D>((j / (NS / 2)) * 32, (j % (NS / 2)) * 16));
@@ -167,6 +179,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       if (j + PF < NS) ring[j % PF] = a_op(j + PF);
       const int kb = j / (NS / 2);
       s[kb] = mfma32(a, qf[j % (NS / 2)], s[kb]);
+      if (j % DMA_GAP == 1 && j / DMA_GAP < DMA_PER_FETCH) dma.issue_one(next_rsrc, next_lds, j / DMA_GAP);
       // Block 1's MFMAs carry block 0's softmax: the max first, then the
       // eight exponential pairs spread over the remaining slots.  Each packed
       // word and the running sum are pinned where they are computed: block
@@ -206,7 +219,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
   };
 
   // Three buffer sets in rotation, the loop unrolled by three.  Tile t+2 is
-  // fetched right after the barrier that retires tile t-1's buffers, so every
+  // fetched during step t, after the barrier that retires tile t-1's buffers, so every
   // tile has two steps to arrive; fetches past the range read zero (an empty
   // resource) and are never used.  Before the barrier a wave waits only for its own loads of
   // tile t: the DMA_PER_FETCH loads of tile t+1 it issued later may stay in
@@ -217,19 +230,19 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     for (int kt = 0;;) {
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 0 complete; buffers 2 no longer read
-      fetch(kt + 2 * BN, ks2, vs2);
+      fetch_spread(kt + 2 * BN, ks2, vs2);
       step(ks0, vs0, kt);
       kt += BN;
       if (kt >= it.k_len) break;
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
-      fetch(kt + 2 * BN, ks0, vs0);
+      fetch_spread(kt + 2 * BN, ks0, vs0);
       step(ks1, vs1, kt);
       kt += BN;
       if (kt >= it.k_len) break;
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 2 complete; buffers 1 no longer read
-      fetch(kt + 2 * BN, ks1, vs1);
+      fetch_spread(kt + 2 * BN, ks1, vs1);
       step(ks2, vs2, kt);
       kt += BN;
       if (kt >= it.k_len) break;

@@ -129,16 +129,27 @@ struct TileDma {
     }
   }
 
-  // Rows [0, ROWS) starting at g_row0; rows at or past nvalid read zero.
-  __device__ __forceinline__ void issue(char* tile, const void* g_row0, int nvalid, uint32_t row_bytes) const {
+  // The resource of rows [0, ROWS) starting at g_row0; rows at or past
+  // nvalid read zero.
+  __device__ __forceinline__ static i32x4 resource(const void* g_row0, int nvalid, uint32_t row_bytes) {
     const int nv = min(nvalid, ROWS);
     const uint32_t bytes = nv > 0 ? (uint32_t)(nv - 1) * row_bytes + D * 2 : 0u;
-    const i32x4 rsrc = buf_rsrc(g_row0, bytes);
+    return buf_rsrc(g_row0, bytes);
+  }
+
+  // This wave's instruction jj (of PER_WAVE) of a fetch into the tile at LDS
+  // address tile_lds.  Issuing a fetch's instructions one at a time between
+  // MFMAs keeps a wave from stalling at issue behind its own burst of DMAs.
+  __device__ __forceinline__ void issue_one(const i32x4& rsrc, uint32_t tile_lds, int jj) const {
+    const int j = min(wave + NW * jj, NJ - 1);
+    dma16(rsrc, voff[jj], __builtin_amdgcn_readfirstlane(tile_lds + j * 1024));
+  }
+
+  // The whole fetch at once.
+  __device__ __forceinline__ void issue(char* tile, const void* g_row0, int nvalid, uint32_t row_bytes) const {
+    const i32x4 rsrc = resource(g_row0, nvalid, row_bytes);
 #pragma unroll
-    for (int jj = 0; jj < PER_WAVE; ++jj) {
-      const int j = min(wave + NW * jj, NJ - 1);
-      dma16(rsrc, voff[jj], __builtin_amdgcn_readfirstlane(lds_addr(tile) + j * 1024));
-    }
+    for (int jj = 0; jj < PER_WAVE; ++jj) issue_one(rsrc, lds_addr(tile), jj);
   }
 };
 
