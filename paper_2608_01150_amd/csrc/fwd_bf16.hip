@@ -173,6 +173,10 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     for (int j = 0; j < PF; ++j) ring[j] = a_op(j);
     s[0] = s[1] = f32x16{};
     __builtin_amdgcn_sched_barrier(0);
+    // Raised issue priority while this wave's MFMA loops run, lowered for the
+    // VALU-only max of block 1: when the SIMD's two waves drift apart, the one
+    // with MFMAs ready issues first and keeps the matrix core fed.
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int j = 0; j < NS; ++j) {
       const u32x4 a = ring[j % PF];
@@ -200,7 +204,9 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     u32x4 cring[PFC];
 #pragma unroll
     for (int m = 0; m < PFC; ++m) cring[m] = c_op(m);
+    __builtin_amdgcn_s_setprio(0);
     block_max(1);
+    __builtin_amdgcn_s_setprio(1);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int m = 0; m < NP; ++m) {
@@ -215,6 +221,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       o[db] = mfma32(a, pb[kb][s2], o[db]);
       __builtin_amdgcn_sched_barrier(0);
     }
+    __builtin_amdgcn_s_setprio(0);
     l_part += lsum;
   };
 
