@@ -80,7 +80,8 @@ enum { ZL_OP_FWD = 0, ZL_OP_BWD = 1, ZL_OP_BWD_DQ = 2 };
  *          empty range yields O_b = 0, LSE_b = -inf.
  * q_offset / k_offset give the global token index of the first row of each
  * segment / range.  They change no value (attention is non-causal, Sec. II-A)
- * and may be NULL; when given they are checked: non-negative, a WHOLE
+ * and may be NULL; when given they are checked: every offset in [0, 2^63 -
+ * 2^31] (so offset + length fits in int64), a WHOLE
  * segment's q_offset equals its range's k_offset, and the blocks of one
  * SHARD cover disjoint global token ranges (overlapping blocks would count
  * keys twice and break exactness).

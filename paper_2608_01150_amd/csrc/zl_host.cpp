@@ -91,6 +91,13 @@ zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_
   if (check_slots && !step_mode && num_slots_arg != nslots)
     return fail(ZL_ERR_INVALID_ARG, "num_slots argument (%d) differs from the descriptor's (%d)",
                 num_slots_arg, nslots);
+  // Offsets, when given: non-negative, and offset + length within int64.
+  constexpr int64_t kOffMax = INT64_MAX - ((int64_t)1 << 31);
+  if (d->k_offset)
+    for (int32_t j = 0; j < nk; ++j)
+      if (d->k_offset[j] < 0 || d->k_offset[j] > kOffMax)
+        return fail(ZL_ERR_INVALID_ARG, "range %d has k_offset %lld outside [0, 2^63 - 2^31]", j,
+                    (long long)d->k_offset[j]);
   std::vector<int32_t> owners(nk, 0);
   Shape sh;
   sh.total_q = d->cu_seqlens_q[nq];
@@ -104,8 +111,9 @@ zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_
     if (c < 1) return fail(ZL_ERR_INVALID_ARG, "segment %d has kv_count %d < 1", s, c);
     if (f < 0 || f > nk - c)
       return fail(ZL_ERR_INVALID_ARG, "segment %d uses ranges [%d, %d) outside [0, %d)", s, f, f + c, nk);
-    if (d->q_offset && d->q_offset[s] < 0)
-      return fail(ZL_ERR_INVALID_ARG, "segment %d has a negative q_offset", s);
+    if (d->q_offset && (d->q_offset[s] < 0 || d->q_offset[s] > kOffMax))
+      return fail(ZL_ERR_INVALID_ARG, "segment %d has q_offset %lld outside [0, 2^63 - 2^31]", s,
+                  (long long)d->q_offset[s]);
     for (int32_t j = f; j < f + c; ++j) owners[j]++;
     if (kind == ZL_WHOLE) {
       if (c != 1) return fail(ZL_ERR_INVALID_ARG, "WHOLE segment %d must use exactly one range", s);
@@ -132,11 +140,10 @@ zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_
             return fail(ZL_ERR_INVALID_ARG, "SHARD segment %d: ranges %d and %d write the same slot %d",
                         s, i, j, b);
         if (d->k_offset) {
-          if (d->k_offset[j] < 0) return fail(ZL_ERR_INVALID_ARG, "range %d has a negative k_offset", j);
           const int64_t a0 = d->k_offset[j], a1 = a0 + (d->cu_seqlens_k[j + 1] - d->cu_seqlens_k[j]);
           for (int32_t i = f; i < j; ++i) {
             const int64_t b0 = d->k_offset[i], b1 = b0 + (d->cu_seqlens_k[i + 1] - d->cu_seqlens_k[i]);
-            if (a0 < b1 && b0 < a1)
+            if (a1 > a0 && b1 > b0 && a0 < b1 && b0 < a1)  // empty blocks cover no token
               return fail(ZL_ERR_INVALID_ARG,
                           "SHARD segment %d: blocks %d and %d overlap in global token positions", s, i, j);
           }
