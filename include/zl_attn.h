@@ -335,7 +335,8 @@ zl_status zl_profile_enable(int32_t on);
 zl_status zl_profile_read(int32_t kernel_id, double* total_ms, int64_t* launches);
 void zl_profile_reset(void);
 
-/* Releases the library's device work-table cache (waits for the device). */
+/* Releases the library's device work-table cache and any pending profiler
+ * events (waits for the device). */
 void zl_shutdown(void);
 
 #ifdef __cplusplus

@@ -460,7 +460,11 @@ hipError_t timed(int kid, hipStream_t s, F&& launch) {
   }
   if (!on) return launch();
   hipEvent_t a = nullptr, b = nullptr;
-  if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return hipErrorOutOfMemory;
+  if (hipEventCreate(&a) != hipSuccess) return hipErrorOutOfMemory;
+  if (hipEventCreate(&b) != hipSuccess) {
+    (void)hipEventDestroy(a);
+    return hipErrorOutOfMemory;
+  }
   (void)hipEventRecord(a, s);
   const hipError_t e = launch();
   (void)hipEventRecord(b, s);
@@ -883,6 +887,7 @@ void zl_profile_reset(void) {
 }
 
 void zl_shutdown(void) {
+  zl_profile_reset();  // retires and destroys any pending timing events
   std::lock_guard<std::mutex> lock(g_mu);
   int cur = 0;
   const bool have_dev = hipGetDevice(&cur) == hipSuccess;
