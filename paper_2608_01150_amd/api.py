@@ -173,6 +173,10 @@ class SegDesc:
         self.num_slots = int(num_slots)
         self.total_q = int(a["cu_seqlens_q"][-1])
         self.total_k = int(a["cu_seqlens_k"][-1])
+        # one past the last packed row of any SHARD segment: the rows a ring
+        # accumulator must cover
+        ends = [int(a["cu_seqlens_q"][s + 1]) for s in range(len(a["kind"])) if int(a["kind"][s]) == ZL_SHARD]
+        self.shard_rows_end = max(ends, default=0)
 
     @classmethod
     def of(cls, w) -> "SegDesc":
@@ -198,6 +202,45 @@ def _p(t: Optional[torch.Tensor]):
     if not t.is_contiguous():
         raise ZlError(ZL_ERR_INVALID_ARG, "tensors must be contiguous")
     return t.data_ptr()
+
+
+def _need(t: Optional[torch.Tensor], name: str, shape, dtype: torch.dtype, min_rows: bool = False) -> None:
+    """Raises ZlError unless `t` (when given) has `shape` (with min_rows: at
+    least shape[0] rows and the rest equal) and `dtype`.  The library reads
+    and writes through raw pointers whose extents follow from the descriptor,
+    so a mismatched tensor must be stopped here."""
+    if t is None:
+        return
+    shape = tuple(int(x) for x in shape)
+    got = tuple(t.shape)
+    if min_rows:
+        ok = len(got) == len(shape) and got[1:] == shape[1:] and got[0] >= shape[0]
+    else:
+        ok = got == shape
+    if not ok:
+        want = f"at least {shape[0]} rows of {shape[1:]}" if min_rows else str(shape)
+        raise ZlError(ZL_ERR_INVALID_ARG, f"{name} has shape {got}, expected {want}")
+    if t.dtype != dtype:
+        raise ZlError(ZL_ERR_INVALID_ARG, f"{name} has dtype {t.dtype}, expected {dtype}")
+
+
+def _same_gpu(*ts) -> torch.device:
+    """The one CUDA device every given tensor is on (raises otherwise)."""
+    devs = {t.device for t in ts if t is not None}
+    if len(devs) != 1 or next(iter(devs)).type != "cuda":
+        raise ZlError(ZL_ERR_INVALID_ARG, f"tensors must all be on one GPU (got {sorted(map(str, devs))})")
+    return next(iter(devs))
+
+
+def _qkv(desc: SegDesc, q, k, v):
+    """Checks q [Tq, H, d] and k, v [Tk, H, d] against the descriptor; returns (H, d)."""
+    if q.dim() != 3:
+        raise ZlError(ZL_ERR_INVALID_ARG, f"q must be [Tq, H, d], got shape {tuple(q.shape)}")
+    _, h, d = q.shape
+    _need(q, "q", (desc.total_q, h, d), q.dtype)
+    _need(k, "k", (desc.total_k, h, d), q.dtype)
+    _need(v, "v", (desc.total_k, h, d), q.dtype)
+    return h, d
 
 
 def _stream(device) -> int:
@@ -249,8 +292,13 @@ def fill_pack(price, mem, load, mem_used, load_floor: float, mem_cap: float):
 
 def attn_fwd(desc: SegDesc, q, k, v, scale: float, out=None, lse=None, o_part=None, lse_part=None):
     """zl_attn_fwd.  Allocates the outputs it is not given; returns (out, lse, o_part, lse_part)."""
-    tq, h, d = q.shape
-    dev = q.device
+    h, d = _qkv(desc, q, k, v)
+    tq = desc.total_q
+    _need(out, "out", (tq, h, d), q.dtype)
+    _need(lse, "lse", (tq, h), torch.float32)
+    _need(o_part, "o_part", (desc.num_slots, tq, h, d), torch.float32)
+    _need(lse_part, "lse_part", (desc.num_slots, tq, h), torch.float32)
+    dev = _same_gpu(q, k, v, out, lse, o_part, lse_part)
     if out is None:
         out = torch.empty_like(q)
     if lse is None:
@@ -268,7 +316,13 @@ def attn_fwd_step(desc: SegDesc, q, k, v, scale: float, out, lse, o_acc, lse_acc
     """zl_attn_fwd_step: one ring step; SHARD rows fold this call's block into (o_acc, lse_acc), and with
     ZL_STEP_LAST write the final out / lse.  Every tensor is caller-provided (o_acc / lse_acc may be None only
     when no SHARD rows need them)."""
-    tq, h, d = q.shape
+    h, d = _qkv(desc, q, k, v)
+    tq, r = desc.total_q, desc.shard_rows_end
+    _need(out, "out", (tq, h, d), q.dtype)
+    _need(lse, "lse", (tq, h), torch.float32)
+    _need(o_acc, "o_acc", (r, h, d), torch.float32, min_rows=True)
+    _need(lse_acc, "lse_acc", (r, h), torch.float32, min_rows=True)
+    _same_gpu(q, k, v, out, lse, o_acc, lse_acc)
     _check(_fwd_step(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
                      _p(o_acc), _p(lse_acc), int(flags), _stream(q.device)))
     return out, lse
@@ -283,9 +337,16 @@ def _cu_rank(cu_rank):
 
 def ulysses_pack_qkv(group: int, q, k, v, send=None):
     """zl_ulysses_pack_qkv: local q, k, v [T, H, d] -> send [group, T, H/group, 3, d]."""
+    if q.dim() != 3:
+        raise ZlError(ZL_ERR_INVALID_ARG, f"q must be [T, H, d], got shape {tuple(q.shape)}")
     t, h, d = q.shape
-    if send is None:
+    if send is None and group >= 1 and h % group == 0:
         send = torch.empty((group, t, h // group, 3, d), dtype=q.dtype, device=q.device)
+    if group >= 1 and h % group == 0:  # otherwise the library reports the bad group
+        _need(k, "k", (t, h, d), q.dtype)
+        _need(v, "v", (t, h, d), q.dtype)
+        _need(send, "send", (group, t, h // group, 3, d), q.dtype)
+        _same_gpu(q, k, v, send)
     _check(_u_pack_qkv(group, t, h, d, _dtype_code(q.dtype), _p(q), _p(k), _p(v), _p(send), _stream(q.device)))
     return send
 
@@ -293,10 +354,18 @@ def ulysses_pack_qkv(group: int, q, k, v, send=None):
 def ulysses_unpack_qkv(group: int, cu_rank, recv, num_heads: int, q=None, k=None, v=None):
     """zl_ulysses_unpack_qkv: rank-major recv [T_full, H/group, 3, d] -> q, k, v [T_full, H/group, d]."""
     cu = _cu_rank(cu_rank)
+    if recv.dim() != 4:
+        raise ZlError(ZL_ERR_INVALID_ARG, f"recv must be [T_full, H/group, 3, d], got shape {tuple(recv.shape)}")
     tf, hl, _, d = recv.shape
     q = torch.empty((tf, hl, d), dtype=recv.dtype, device=recv.device) if q is None else q
     k = torch.empty_like(q) if k is None else k
     v = torch.empty_like(q) if v is None else v
+    if group >= 1 and num_heads % group == 0 and cu.shape[0] == group:
+        t_full = int(cu[:, -1].sum())
+        _need(recv, "recv", (t_full, num_heads // group, 3, d), recv.dtype)
+        for t, name in ((q, "q"), (k, "k"), (v, "v")):
+            _need(t, name, (t_full, num_heads // group, d), recv.dtype)
+        _same_gpu(recv, q, k, v)
     _check(_u_unpack_qkv(group, cu.shape[1] - 1, cu.ctypes.data_as(_i32p), num_heads, d, _dtype_code(recv.dtype),
                          _p(recv), _p(q), _p(k), _p(v), _stream(recv.device)))
     return q, k, v
@@ -305,7 +374,14 @@ def ulysses_unpack_qkv(group: int, cu_rank, recv, num_heads: int, q=None, k=None
 def ulysses_pack_out(group: int, cu_rank, out, num_heads: int, send=None):
     """zl_ulysses_pack_out: out [T_full, H/group, d] -> rank-major send [T_full, H/group, d]."""
     cu = _cu_rank(cu_rank)
+    if out.dim() != 3:
+        raise ZlError(ZL_ERR_INVALID_ARG, f"out must be [T_full, H/group, d], got shape {tuple(out.shape)}")
     send = torch.empty_like(out) if send is None else send
+    if group >= 1 and num_heads % group == 0 and cu.shape[0] == group:
+        shape = (int(cu[:, -1].sum()), num_heads // group, out.shape[2])
+        _need(out, "out", shape, out.dtype)
+        _need(send, "send", shape, out.dtype)
+        _same_gpu(out, send)
     _check(_u_pack_out(group, cu.shape[1] - 1, cu.ctypes.data_as(_i32p), num_heads, out.shape[2],
                        _dtype_code(out.dtype), _p(out), _p(send), _stream(out.device)))
     return send
@@ -313,9 +389,15 @@ def ulysses_pack_out(group: int, cu_rank, out, num_heads: int, send=None):
 
 def ulysses_unpack_out(group: int, recv, num_heads: int, out_local=None):
     """zl_ulysses_unpack_out: recv [group, T, H/group, d] -> out_local [T, H, d]."""
+    if recv.dim() != 4:
+        raise ZlError(ZL_ERR_INVALID_ARG, f"recv must be [group, T, H/group, d], got shape {tuple(recv.shape)}")
     g, t, hl, d = recv.shape
     if out_local is None:
         out_local = torch.empty((t, num_heads, d), dtype=recv.dtype, device=recv.device)
+    if group >= 1 and num_heads % group == 0:
+        _need(recv, "recv", (group, t, num_heads // group, d), recv.dtype)
+        _need(out_local, "out_local", (t, num_heads, d), recv.dtype)
+        _same_gpu(recv, out_local)
     _check(_u_unpack_out(group, t, num_heads, d, _dtype_code(recv.dtype), _p(recv), _p(out_local),
                          _stream(recv.device)))
     return out_local
@@ -323,7 +405,15 @@ def ulysses_unpack_out(group: int, recv, num_heads: int, out_local=None):
 
 def lse_merge(desc: SegDesc, o_part, lse_part, out, lse):
     """zl_lse_merge: writes the SHARD rows of out / lse."""
-    tq, h, d = out.shape
+    if out.dim() != 3:
+        raise ZlError(ZL_ERR_INVALID_ARG, f"out must be [Tq, H, d], got shape {tuple(out.shape)}")
+    _, h, d = out.shape
+    tq = desc.total_q
+    _need(out, "out", (tq, h, d), out.dtype)
+    _need(lse, "lse", (tq, h), torch.float32)
+    _need(o_part, "o_part", (desc.num_slots, tq, h, d), torch.float32)
+    _need(lse_part, "lse_part", (desc.num_slots, tq, h), torch.float32)
+    _same_gpu(out, lse, o_part, lse_part)
     _check(_merge(desc.ptr(), h, d, _dtype_code(out.dtype), _p(o_part), _p(lse_part), desc.num_slots, _p(out),
                   _p(lse), _stream(out.device)))
     return out, lse
@@ -331,26 +421,40 @@ def lse_merge(desc: SegDesc, o_part, lse_part, out, lse):
 
 def attn_bwd(desc: SegDesc, q, k, v, out, lse, dout, scale: float, dq=None, dk=None, dv=None, workspace=None):
     """zl_attn_bwd.  Allocates dq/dk/dv/workspace it is not given; returns (dq, dk, dv)."""
-    tq, h, d = q.shape
-    dev = q.device
+    h, d = _qkv(desc, q, k, v)
+    tq, tk = desc.total_q, desc.total_k
+    for t, name in ((out, "out"), (dout, "dout"), (dq, "dq")):
+        _need(t, name, (tq, h, d), q.dtype)
+    for t, name in ((dk, "dk"), (dv, "dv")):
+        _need(t, name, (tk, h, d), q.dtype)
+    _need(lse, "lse", (tq, h), torch.float32)
+    dev = _same_gpu(q, k, v, out, lse, dout, dq, dk, dv, workspace)
     dq = torch.empty_like(q) if dq is None else dq
     dk = torch.zeros_like(k) if dk is None else dk
     dv = torch.zeros_like(v) if dv is None else dv
     if workspace is None:
         workspace = torch.empty(workspace_size(desc, h, d, q.dtype, ZL_OP_BWD), dtype=torch.uint8, device=dev)
     _check(_bwd(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
-                _p(dout), _p(dq), _p(dk), _p(dv), 0, _p(workspace), workspace.numel(), _stream(dev)))
+                _p(dout), _p(dq), _p(dk), _p(dv), 0, _p(workspace), workspace.numel() * workspace.element_size(), _stream(dev)))
     return dq, dk, dv
 
 
 def attn_bwd_step(desc: SegDesc, q, k, v, out, lse, dout, scale: float, dq, dk, dv, dq_acc, flags: int,
                   workspace=None):
     """zl_attn_bwd_step: one ring step of the backward (see the header); returns (dq, dk, dv)."""
-    tq, h, d = q.shape
+    h, d = _qkv(desc, q, k, v)
+    tq, tk = desc.total_q, desc.total_k
+    for t, name in ((out, "out"), (dout, "dout"), (dq, "dq")):
+        _need(t, name, (tq, h, d), q.dtype)
+    for t, name in ((dk, "dk"), (dv, "dv")):
+        _need(t, name, (tk, h, d), q.dtype)
+    _need(lse, "lse", (tq, h), torch.float32)
+    _need(dq_acc, "dq_acc", (desc.shard_rows_end, h, d), torch.float32, min_rows=True)
+    _same_gpu(q, k, v, out, lse, dout, dq, dk, dv, dq_acc, workspace)
     if workspace is None:
         workspace = torch.empty(workspace_size(desc, h, d, q.dtype, ZL_OP_BWD), dtype=torch.uint8, device=q.device)
     _check(_bwd_step(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
-                     _p(dout), _p(dq), _p(dk), _p(dv), _p(dq_acc), int(flags), _p(workspace), workspace.numel(),
+                     _p(dout), _p(dq), _p(dk), _p(dv), _p(dq_acc), int(flags), _p(workspace), workspace.numel() * workspace.element_size(),
                      _stream(q.device)))
     return dq, dk, dv
 
