@@ -32,7 +32,10 @@
  *   - The library owns one cache of device work tables (the schedule of a
  *     descriptor), created on the first call with a new descriptor, reused
  *     afterwards and released by zl_shutdown().  It allocates no other
- *     device memory.
+ *     device memory.  Once a descriptor's tables exist, calls with it only
+ *     launch kernels (no allocation, copy, memset or synchronisation), so
+ *     they may be captured in a HIP graph; make the first call eagerly, and
+ *     keep profiling off while capturing.
  */
 #ifndef ZL_ATTN_H
 #define ZL_ATTN_H
