@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c4", help="c2..c5 (default c4: coalesced whole+shard)")
     ap.add_argument("--ulysses-group", type=int, default=8, help="group size h for --mode ulysses")
+    ap.add_argument("--partials", default="fp32", choices=("fp32", "bf16"),
+                    help="--mode blocks: dtype of the shard partials between the forward and the merge "
+                         "(bf16 halves their bytes and rounds each block's output once more)")
     ap.add_argument("--mode", default="blocks", choices=("blocks", "ring", "gather", "ulysses"),
                     help="how a shard's K/V blocks reach the forward: blocks = all blocks in one launch plus "
                          "the LSE merge (default); ring = one ring step per block with the merge fused into "
@@ -261,7 +264,8 @@ def main():
     lse = torch.empty((w.total_q, H), dtype=torch.float32, device=dev)
     o_part = lse_part = None
     if w.num_slots:
-        o_part = torch.empty((w.num_slots, w.total_q, H, hd), dtype=torch.float32, device=dev)
+        pdt = torch.bfloat16 if args.partials == "bf16" else torch.float32
+        o_part = torch.empty((w.num_slots, w.total_q, H, hd), dtype=pdt, device=dev)
         lse_part = torch.empty((w.num_slots, w.total_q, H), dtype=torch.float32, device=dev)
     dq = torch.empty_like(q)
     dk = torch.empty_like(k)
@@ -400,7 +404,8 @@ def main():
     if w.num_slots and avg.get("merge"):
         sr = w.shard_rows()
         nb = max(w.kv_count[s] for s in range(w.num_segments) if w.kind[s] == W.SHARD)
-        mbytes = H * sr * (nb * (4 * hd + 4) + 2 * hd + 4)
+        pb = 2 if args.partials == "bf16" else 4   # bytes per partial element
+        mbytes = H * sr * (nb * (pb * hd + 4) + 2 * hd + 4)
         gbs = mbytes / (avg["merge"] * 1e-3) / 1e9
         rec["merge_kernel"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": mbytes}
@@ -410,6 +415,8 @@ def main():
     for op in (api.ZL_OP_FWD, api.ZL_OP_BWD, api.ZL_OP_BWD_DQ):
         api.plan_dump(desc, H, hd, q.dtype, op)
     rec["host_scheduler_ms"] = round((time.perf_counter() - t0) * 1e3, 3)
+    if args.mode == "blocks" and w.num_slots:
+        rec["config"]["partials"] = args.partials
     if args.mode == "ulysses":
         total_b = sum(ulysses_bytes.values())
         ums = avg.get("ulysses", 0.0)

@@ -136,6 +136,20 @@ zl_status zl_attn_fwd(const zl_seg_desc* desc, int32_t num_heads, int32_t head_d
                       void* out, float* lse, float* o_part, float* lse_part, int32_t num_slots,
                       void* stream);
 
+/*
+ * zl_attn_fwd with the SHARD partials stored in `part_dtype`: ZL_FP32 (as
+ * zl_attn_fwd) or ZL_BF16, which rounds each block-normalised O_b once to
+ * bf16 and halves the partial bytes written here and read by the merge (the
+ * final O is then rounded twice: O_b, then the merged result).  o_part is
+ * [num_slots, Tq, H, d] of that type; lse_part stays fp32.  ZL_BF16 partials
+ * need dtype ZL_BF16 (ZL_ERR_UNSUPPORTED otherwise); an unknown part_dtype
+ * is ZL_ERR_INVALID_ARG.  Everything else as zl_attn_fwd.
+ */
+zl_status zl_attn_fwd_ex(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
+                         float softmax_scale, const void* q, const void* k, const void* v,
+                         void* out, float* lse, void* o_part, zl_dtype part_dtype, float* lse_part,
+                         int32_t num_slots, void* stream);
+
 /* Flags of zl_attn_fwd_step. */
 #define ZL_STEP_FIRST 1u /* this call carries every SHARD row's first block */
 #define ZL_STEP_LAST 2u  /* this call carries every SHARD row's last block */
@@ -221,6 +235,12 @@ zl_status zl_ulysses_unpack_out(int32_t group, int32_t t_local, int32_t num_head
 zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype out_dtype,
                        const float* o_part, const float* lse_part, int32_t num_slots,
                        void* out, float* lse, void* stream);
+
+/* zl_lse_merge reading partials of `part_dtype` (ZL_FP32 or ZL_BF16, as
+ * written by zl_attn_fwd_ex); otherwise identical. */
+zl_status zl_lse_merge_ex(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype out_dtype,
+                          const void* o_part, zl_dtype part_dtype, const float* lse_part, int32_t num_slots,
+                          void* out, float* lse, void* stream);
 
 /*
  * Backward of the packed batch.  `out` and `lse` are the FINAL outputs (for

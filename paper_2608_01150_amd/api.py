@@ -75,6 +75,8 @@ _workspace_size = _sig("zl_workspace_size", ctypes.c_int, _DP, ctypes.c_int32, c
                        ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t))
 _fwd = _sig("zl_attn_fwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
             _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp)
+_fwd_ex = _sig("zl_attn_fwd_ex", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
+               _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_int, _vp, ctypes.c_int32, _vp)
 _fwd_step = _sig("zl_attn_fwd_step", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
                  _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_uint32, _vp)
 _u_pack_qkv = _sig("zl_ulysses_pack_qkv", ctypes.c_int, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -87,6 +89,8 @@ _u_unpack_out = _sig("zl_ulysses_unpack_out", ctypes.c_int, ctypes.c_int32, ctyp
                      ctypes.c_int32, ctypes.c_int, _vp, _vp, _vp)
 _merge = _sig("zl_lse_merge", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, _vp, _vp,
               ctypes.c_int32, _vp, _vp, _vp)
+_merge_ex = _sig("zl_lse_merge_ex", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, _vp, ctypes.c_int,
+                 _vp, ctypes.c_int32, _vp, _vp, _vp)
 _bwd = _sig("zl_attn_bwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
             _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_uint32, _vp, ctypes.c_size_t, _vp)
 _bwd_step = _sig("zl_attn_bwd_step", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
@@ -290,13 +294,19 @@ def fill_pack(price, mem, load, mem_used, load_floor: float, mem_cap: float):
     return rank_of, ld, mu, (None if failed.value < 0 else int(failed.value))
 
 
-def attn_fwd(desc: SegDesc, q, k, v, scale: float, out=None, lse=None, o_part=None, lse_part=None):
-    """zl_attn_fwd.  Allocates the outputs it is not given; returns (out, lse, o_part, lse_part)."""
+def attn_fwd(desc: SegDesc, q, k, v, scale: float, out=None, lse=None, o_part=None, lse_part=None,
+             part_dtype: Optional[torch.dtype] = None):
+    """zl_attn_fwd (fp32 partials) or zl_attn_fwd_ex (bf16 partials).  The partials' dtype is o_part's,
+    else part_dtype (default fp32).  Allocates the outputs it is not given; returns (out, lse, o_part,
+    lse_part)."""
     h, d = _qkv(desc, q, k, v)
     tq = desc.total_q
+    pdt = o_part.dtype if o_part is not None else (part_dtype or torch.float32)
+    if pdt not in (torch.float32, torch.bfloat16):
+        raise ZlError(ZL_ERR_INVALID_ARG, f"partials must be float32 or bfloat16, got {pdt}")
     _need(out, "out", (tq, h, d), q.dtype)
     _need(lse, "lse", (tq, h), torch.float32)
-    _need(o_part, "o_part", (desc.num_slots, tq, h, d), torch.float32)
+    _need(o_part, "o_part", (desc.num_slots, tq, h, d), pdt)
     _need(lse_part, "lse_part", (desc.num_slots, tq, h), torch.float32)
     dev = _same_gpu(q, k, v, out, lse, o_part, lse_part)
     if out is None:
@@ -304,11 +314,15 @@ def attn_fwd(desc: SegDesc, q, k, v, scale: float, out=None, lse=None, o_part=No
     if lse is None:
         lse = torch.empty((tq, h), dtype=torch.float32, device=dev)
     if o_part is None and desc.num_slots > 0:
-        o_part = torch.empty((desc.num_slots, tq, h, d), dtype=torch.float32, device=dev)
+        o_part = torch.empty((desc.num_slots, tq, h, d), dtype=pdt, device=dev)
     if lse_part is None and desc.num_slots > 0:
         lse_part = torch.empty((desc.num_slots, tq, h), dtype=torch.float32, device=dev)
-    _check(_fwd(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
-                _p(o_part), _p(lse_part), desc.num_slots, _stream(dev)))
+    if pdt == torch.float32:
+        _check(_fwd(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
+                    _p(o_part), _p(lse_part), desc.num_slots, _stream(dev)))
+    else:
+        _check(_fwd_ex(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
+                       _p(o_part), ZL_BF16, _p(lse_part), desc.num_slots, _stream(dev)))
     return out, lse, o_part, lse_part
 
 
@@ -404,18 +418,25 @@ def ulysses_unpack_out(group: int, recv, num_heads: int, out_local=None):
 
 
 def lse_merge(desc: SegDesc, o_part, lse_part, out, lse):
-    """zl_lse_merge: writes the SHARD rows of out / lse."""
+    """zl_lse_merge (zl_lse_merge_ex for bf16 o_part): writes the SHARD rows of out / lse."""
     if out.dim() != 3:
         raise ZlError(ZL_ERR_INVALID_ARG, f"out must be [Tq, H, d], got shape {tuple(out.shape)}")
     _, h, d = out.shape
     tq = desc.total_q
     _need(out, "out", (tq, h, d), out.dtype)
     _need(lse, "lse", (tq, h), torch.float32)
-    _need(o_part, "o_part", (desc.num_slots, tq, h, d), torch.float32)
+    pdt = o_part.dtype if o_part is not None else torch.float32
+    if pdt not in (torch.float32, torch.bfloat16):
+        raise ZlError(ZL_ERR_INVALID_ARG, f"partials must be float32 or bfloat16, got {pdt}")
+    _need(o_part, "o_part", (desc.num_slots, tq, h, d), pdt)
     _need(lse_part, "lse_part", (desc.num_slots, tq, h), torch.float32)
     _same_gpu(out, lse, o_part, lse_part)
-    _check(_merge(desc.ptr(), h, d, _dtype_code(out.dtype), _p(o_part), _p(lse_part), desc.num_slots, _p(out),
-                  _p(lse), _stream(out.device)))
+    if pdt == torch.float32:
+        _check(_merge(desc.ptr(), h, d, _dtype_code(out.dtype), _p(o_part), _p(lse_part), desc.num_slots, _p(out),
+                      _p(lse), _stream(out.device)))
+    else:
+        _check(_merge_ex(desc.ptr(), h, d, _dtype_code(out.dtype), _p(o_part), ZL_BF16, _p(lse_part), desc.num_slots,
+                         _p(out), _p(lse), _stream(out.device)))
     return out, lse
 
 

@@ -18,7 +18,8 @@
 // staging costs half as much per MFMA as with 128-row items.
 //
 // Epilogue: WHOLE items write the final bf16 output and the LSE; SHARD items
-// write the block-normalised fp32 partial and its LSE into their CP slot.
+// write the block-normalised partial (fp32, or bf16 on request) and its LSE
+// into their CP slot.
 
 #include "zl_device.h"
 #include "zl_internal.h"
@@ -308,8 +309,22 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       }
     }
     if (g == 0) (p.step_last ? p.lse : p.lse_acc)[row] = lse_new;
+  } else if (p.part_bf16) {
+    // bf16 partial: this lane's 8 consecutive d values in one 16-byte store
+    uint16_t* og = static_cast<uint16_t*>(p.o_part) + it.slot * p.slot_stride + row * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        u32x4 w;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[t] = pack_bf16(o[db][8 * h + 2 * t] * inv, o[db][8 * h + 2 * t + 1] * inv);
+        *reinterpret_cast<u32x4*>(og + db * 32 + 16 * h + 8 * g) = w;
+      }
+    }
+    if (g == 0) p.lse_part[it.slot * p.lse_slot_stride + row] = lse;
   } else {
-    float* og = p.o_part + it.slot * p.slot_stride + row * D;
+    float* og = static_cast<float*>(p.o_part) + it.slot * p.slot_stride + row * D;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
 #pragma unroll

@@ -82,7 +82,7 @@ __global__ __launch_bounds__(BM) void fwd_fp32_kernel(FwdParams p) {
     (p.step_last ? p.lse : p.lse_acc)[row] = lse_new;
     return;
   }
-  float* og = it.slot < 0 ? static_cast<float*>(p.out) + row * D : p.o_part + it.slot * p.slot_stride + row * D;
+  float* og = it.slot < 0 ? static_cast<float*>(p.out) + row * D : static_cast<float*>(p.o_part) + it.slot * p.slot_stride + row * D;
 #pragma unroll
   for (int c = 0; c < D; c += 4) {
     *reinterpret_cast<f32x4*>(og + c) = f32x4{o[c] * inv, o[c + 1] * inv, o[c + 2] * inv, o[c + 3] * inv};

@@ -516,8 +516,17 @@ zl_status zl_workspace_size(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_d
 zl_status zl_attn_fwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
                       const void* k, const void* v, void* out, float* lse, float* o_part, float* lse_part,
                       int32_t num_slots, void* stream) {
+  return zl_attn_fwd_ex(desc, H, hd, dt, scale, q, k, v, out, lse, o_part, ZL_FP32, lse_part, num_slots, stream);
+}
+
+zl_status zl_attn_fwd_ex(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
+                         const void* k, const void* v, void* out, float* lse, void* o_part, zl_dtype part_dt,
+                         float* lse_part, int32_t num_slots, void* stream) {
   zl_status st = validate_common(H, hd, dt, scale, true);
   if (st != ZL_OK) return st;
+  if (part_dt != ZL_FP32 && part_dt != ZL_BF16) return fail(ZL_ERR_INVALID_ARG, "unknown partial dtype %d", (int)part_dt);
+  if (part_dt == ZL_BF16 && dt != ZL_BF16)
+    return fail(ZL_ERR_UNSUPPORTED, "bf16 partials need a bf16 forward");
   Shape sh;
   if ((st = validate_desc(desc, num_slots, true, &sh)) != ZL_OK) return st;
   if ((st = check_sizes(sh, H, hd, num_slots)) != ZL_OK) return st;
@@ -542,6 +551,7 @@ zl_status zl_attn_fwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype d
   p.out = out;
   p.lse = lse;
   p.o_part = o_part;
+  p.part_bf16 = part_dt == ZL_BF16 ? 1 : 0;
   p.lse_part = lse_part;
   p.items = static_cast<const zl::Item*>(plan->dev);
   p.n_items = plan->n_items;
@@ -700,8 +710,15 @@ zl_status zl_ulysses_unpack_out(int32_t group, int32_t t_local, int32_t H, int32
 
 zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype out_dt, const float* o_part,
                        const float* lse_part, int32_t num_slots, void* out, float* lse, void* stream) {
+  return zl_lse_merge_ex(desc, H, hd, out_dt, o_part, ZL_FP32, lse_part, num_slots, out, lse, stream);
+}
+
+zl_status zl_lse_merge_ex(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype out_dt, const void* o_part,
+                          zl_dtype part_dt, const float* lse_part, int32_t num_slots, void* out, float* lse,
+                          void* stream) {
   zl_status st = validate_common(H, hd, out_dt, 1.f, false);
   if (st != ZL_OK) return st;
+  if (part_dt != ZL_FP32 && part_dt != ZL_BF16) return fail(ZL_ERR_INVALID_ARG, "unknown partial dtype %d", (int)part_dt);
   Shape sh;
   if ((st = validate_desc(desc, num_slots, true, &sh)) != ZL_OK) return st;
   if ((st = check_sizes(sh, H, hd, num_slots)) != ZL_OK) return st;
@@ -726,8 +743,9 @@ zl_status zl_lse_merge(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype 
   p.n_units = plan->n_units;
   p.slot_stride = (int64_t)sh.total_q * H * hd;
   p.lse_slot_stride = (int64_t)sh.total_q * H;
-  return hip_status(timed(ZL_K_MERGE, s, [&] { return zl::launch_merge(p, hd, out_dt == ZL_BF16, s); }),
-                    "merge launch");
+  return hip_status(
+      timed(ZL_K_MERGE, s, [&] { return zl::launch_merge(p, hd, out_dt == ZL_BF16, part_dt == ZL_BF16, s); }),
+      "merge launch");
 }
 
 }  // extern "C"

@@ -55,7 +55,7 @@ struct FwdParams {
   const void* v;
   void* out;
   float* lse;
-  float* o_part;
+  void* o_part;          // [S, Tq, H, d] fp32, or bf16 when part_bf16
   float* lse_part;
   const Item* items;
   int32_t n_items;
@@ -72,6 +72,7 @@ struct FwdParams {
   int32_t step_last;     // the combined result goes to out / lse
   float* o_acc;          // [Tq, H, d] fp32
   float* lse_acc;        // [Tq, H] fp32
+  int32_t part_bf16;     // SHARD partials stored as bf16 (rounded once) instead of fp32
 };
 
 struct MergeSeg {
@@ -80,7 +81,7 @@ struct MergeSeg {
 };
 
 struct MergeParams {
-  const float* o_part;
+  const void* o_part;    // fp32, or bf16 (launch_merge's part_bf16)
   const float* lse_part;
   void* out;
   float* lse;
@@ -141,7 +142,7 @@ struct UlyssesParams {
   int32_t group;
 };
 
-hipError_t launch_merge(const MergeParams& p, int head_dim, bool out_bf16, hipStream_t s);
+hipError_t launch_merge(const MergeParams& p, int head_dim, bool out_bf16, bool part_bf16, hipStream_t s);
 hipError_t launch_ulysses(const UlyssesParams& p, int op, int head_dim, hipStream_t s);
 // stage 0: preprocess (D), 1: dK/dV, 2: dQ
 hipError_t launch_bwd_bf16(const BwdParams& p, int head_dim, int stage, hipStream_t s);

@@ -24,7 +24,8 @@ def test_exports_every_declared_symbol():
     assert {"zl_attn_fwd", "zl_attn_bwd", "zl_lse_merge", "zl_plan_dump", "zl_workspace_size",
             "zl_last_error", "zl_abi_version", "zl_shutdown", "zl_profile_enable", "zl_profile_read",
             "zl_profile_reset", "zl_attn_fwd_step", "zl_ulysses_pack_qkv", "zl_ulysses_unpack_qkv",
-            "zl_ulysses_pack_out", "zl_ulysses_unpack_out", "zl_fill_pack", "zl_attn_bwd_step"} <= set(names)
+            "zl_ulysses_pack_out", "zl_ulysses_unpack_out", "zl_fill_pack", "zl_attn_bwd_step",
+            "zl_attn_fwd_ex", "zl_lse_merge_ex"} <= set(names)
     for n in names:
         assert hasattr(api._lib, n), n
 
@@ -196,3 +197,16 @@ def test_ulysses_rules():
     empty = np.zeros((2, 3), np.int32)
     assert api._u_unpack_qkv(2, 2, empty.ctypes.data_as(api._i32p), 8, 128, api.ZL_BF16, None, None, None, None,
                              None) == api.ZL_OK
+
+
+def test_partial_dtype_rules():
+    """zl_attn_fwd_ex / zl_lse_merge_ex reject an unknown partial dtype, and bf16 partials of an fp32
+    forward, before looking at anything else."""
+    d = _ok_desc()
+    ptrs = (FAKE,) * 5
+    st = api._fwd_ex(d.ptr(), 2, 64, api.ZL_BF16, 0.125, *ptrs, FAKE, 7, FAKE, d.num_slots, None)
+    assert st == api.ZL_ERR_INVALID_ARG and "partial dtype" in api.last_error()
+    st = api._fwd_ex(d.ptr(), 2, 64, api.ZL_FP32, 0.125, *ptrs, FAKE, api.ZL_BF16, FAKE, d.num_slots, None)
+    assert st == api.ZL_ERR_UNSUPPORTED and "bf16 partials" in api.last_error()
+    st = api._merge_ex(d.ptr(), 2, 64, api.ZL_BF16, FAKE, 9, FAKE, d.num_slots, FAKE, FAKE, None)
+    assert st == api.ZL_ERR_INVALID_ARG and "partial dtype" in api.last_error()

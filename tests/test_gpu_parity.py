@@ -60,7 +60,7 @@ def _shard_rows_slots(d):
     return out
 
 
-def run_and_compare(d, H, hd, dtype, seed, backward=True, scale=None):
+def run_and_compare(d, H, hd, dtype, seed, backward=True, scale=None, part_dtype=torch.float32):
     desc = api.SegDesc.of(d)
     q, k, v, do = _inputs(d, H, hd, dtype, seed)
     scale = 1.0 / hd ** 0.5 if scale is None else scale
@@ -69,7 +69,7 @@ def run_and_compare(d, H, hd, dtype, seed, backward=True, scale=None):
     nan = float("nan")
     out = torch.full_like(qd, nan)
     lse = torch.full((tq, H), nan, device="cuda")
-    o_part = torch.full((max(desc.num_slots, 1), tq, H, hd), nan, device="cuda")
+    o_part = torch.full((max(desc.num_slots, 1), tq, H, hd), nan, dtype=part_dtype, device="cuda")
     lse_part = torch.full((max(desc.num_slots, 1), tq, H), nan, device="cuda")
     api.attn_fwd(desc, qd, kd_, vd, scale, out, lse, o_part if desc.num_slots else None,
                  lse_part if desc.num_slots else None)
@@ -111,6 +111,25 @@ def run_and_compare(d, H, hd, dtype, seed, backward=True, scale=None):
         _check_bwd(dk, rk, "dk")
         _check_bwd(dv, rv, "dv")
     return out, lse
+
+
+@pytest.mark.parametrize("hd", [64, 128])
+def test_bf16_partials(hd):
+    """Partials stored in bf16 (zl_attn_fwd_ex / zl_lse_merge_ex): each O_b is rounded once more, the
+    same bf16 tolerances against the oracle hold, and the merged output stays within that tolerance of the
+    fp32-partial path's (an absolute bound: blocks may cancel, so |O| can be far below |O_b|)."""
+    d = _descs.mixed_small()
+    out_b, lse_b = run_and_compare(d, 3, hd, torch.bfloat16, 41 + hd, backward=False, part_dtype=torch.bfloat16)
+    out_f, lse_f = run_and_compare(d, 3, hd, torch.bfloat16, 41 + hd, backward=False)
+    assert torch.equal(lse_b, lse_f)  # the LSE partials stay fp32
+    assert (out_b.float() - out_f.float()).abs().max().item() <= O_TOL
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_bf16_partials_random_descriptors(seed):
+    rng = np.random.default_rng(700 + seed)
+    d = _descs.random_desc(rng, int(rng.integers(0, 3)), int(rng.integers(1, 4)), 300, 5)
+    run_and_compare(d, 2, 128, torch.bfloat16, 90 + seed, backward=True, part_dtype=torch.bfloat16)
 
 
 def test_mfma_layout_probe_free_smoke():
