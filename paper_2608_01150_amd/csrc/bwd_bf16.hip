@@ -479,6 +479,17 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
     }
   };
 
+  // Waves with no query rows skip the math (see the forward kernel).
+  const bool wave_live = wave * 32 < it.q_len;
+  auto run = [&](const char* kbuf, const char* vbuf) __attribute__((always_inline)) {
+    if (wave_live) {
+      step(kbuf, vbuf);
+    } else {
+#pragma unroll
+      for (int jj = 0; jj < DMA_PER_FETCH; ++jj) dma.issue_one(next_rsrc, next_lds, jj);
+    }
+  };
+
   // Three buffer sets in rotation, unrolled by three, as in the forward.
   if (it.k_len > 0) {
     fetch(0, ks0, vs0);
@@ -487,19 +498,19 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 0 complete; buffers 2 no longer read
       fetch_spread(kt + 2 * BN, ks2, vs2);
-      step(ks0, vs0);
+      run(ks0, vs0);
       kt += BN;
       if (kt >= it.k_len) break;
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
       fetch_spread(kt + 2 * BN, ks0, vs0);
-      step(ks1, vs1);
+      run(ks1, vs1);
       kt += BN;
       if (kt >= it.k_len) break;
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 2 complete; buffers 1 no longer read
       fetch_spread(kt + 2 * BN, ks1, vs1);
-      step(ks2, vs2);
+      run(ks2, vs2);
       kt += BN;
       if (kt >= it.k_len) break;
     }

@@ -226,6 +226,20 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     l_part += lsum;
   };
 
+  // A wave with no query rows in this item (the ragged last tile of a
+  // segment) skips the math and only issues its share of the next tile's
+  // loads, which the other waves need; the SIMD's other wave then has the
+  // matrix core to itself.
+  const bool wave_live = wave * 32 < it.q_len;
+  auto run = [&](const char* kbuf, const char* vbuf, int kt) __attribute__((always_inline)) {
+    if (wave_live) {
+      step(kbuf, vbuf, kt);
+    } else {
+#pragma unroll
+      for (int jj = 0; jj < DMA_PER_FETCH; ++jj) dma.issue_one(next_rsrc, next_lds, jj);
+    }
+  };
+
   // Three buffer sets in rotation, the loop unrolled by three.  Tile t+2 is
   // fetched during step t, after the barrier that retires tile t-1's buffers, so every
   // tile has two steps to arrive; fetches past the range read zero (an empty
@@ -239,19 +253,19 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 0 complete; buffers 2 no longer read
       fetch_spread(kt + 2 * BN, ks2, vs2);
-      step(ks0, vs0, kt);
+      run(ks0, vs0, kt);
       kt += BN;
       if (kt >= it.k_len) break;
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
       fetch_spread(kt + 2 * BN, ks0, vs0);
-      step(ks1, vs1, kt);
+      run(ks1, vs1, kt);
       kt += BN;
       if (kt >= it.k_len) break;
       wait_vmem_keep<DMA_PER_FETCH>();
       __syncthreads();  // tile in buffers 2 complete; buffers 1 no longer read
       fetch_spread(kt + 2 * BN, ks1, vs1);
-      step(ks2, vs2, kt);
+      run(ks2, vs2, kt);
       kt += BN;
       if (kt >= it.k_len) break;
     }
