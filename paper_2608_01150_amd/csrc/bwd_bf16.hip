@@ -157,7 +157,13 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
     // or dO (odd j) chunk j/2 of the sub-block's 32 rows.  Sub-block k is half
     // ka = k % 2 of the tile in buffer b; B(k-1) is half sbb of the tile in
     // buffer bb (all literals at the call sites).
+    // A producer whose key group holds no key of the item (the ragged last
+    // tile of a segment) skips its phases: their exchange words would only
+    // feed the dK/dV of keys past the range, which are never stored.  Its
+    // tile loads and barriers are outside the phases and still run.
+    const bool live = kw * 32 < it.k_len;
     auto phase = [&](int ka, int b, int sbb, int bb, bool has_b, int xb) __attribute__((always_inline)) {
+      if (!live) return;
       const char* qa = qs[b] + a_off + 32 * ka * PITCH;
       const char* oa = dos[b] + a_off + 32 * ka * PITCH;
       auto a_op = [&](int j) { return *reinterpret_cast<const u32x4*>(((j & 1) ? oa : qa) + poff<D>(0, (j >> 1) * 16)); };
