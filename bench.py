@@ -197,8 +197,9 @@ def ring_bwd_steps(w, q, k, v, out, lse, do, dq, dk, dv):
     return steps
 
 
-# Source files whose text determines each kernel's code; a stored counter
-# measurement applies only while their hash is unchanged.
+# Source files whose text (with the compile flags applied to them) determines
+# each kernel's code; a stored counter measurement applies only while their
+# hash is unchanged.
 KERNEL_SOURCES = {
     "fwd": ["fwd_bf16.hip"],
     "bwd_dkdv": ["bwd_bf16.hip"],
@@ -212,10 +213,15 @@ TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profile
 def kernel_source_hash(kernel: str) -> str:
     import hashlib
     csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_01150_amd", "csrc")
+    from paper_2608_01150_amd import build as _build
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[kernel] + COMMON_SOURCES:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
+    flags = [a for a in _build.HIP_FLAGS if not a.startswith("/")]  # include paths vary by checkout
+    for f in KERNEL_SOURCES[kernel]:
+        flags += getattr(_build, "FILE_FLAGS", {}).get(f, [])
+    h.update("\0".join(flags).encode())
     return h.hexdigest()
 
 

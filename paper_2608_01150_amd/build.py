@@ -21,6 +21,12 @@ HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contra
              "-I", INCLUDE, "-I", CSRC]
 
 
+# Per-source flags.  The forward's row max is a chain of fmaxf; without NaN
+# operands (masked keys are -inf, which stays honoured) it lowers to bare
+# v_max/v_max3, saving the NaN-quieting self-max ops (about 8% of its VALU).
+FILE_FLAGS = {"fwd_bf16.hip": ["-fno-honor-nans"]}
+
+
 def _hipcc():
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if cand and os.path.exists(cand):
@@ -30,7 +36,7 @@ def _hipcc():
 
 def _compile(src: str, extra) -> str:
     obj = os.path.join(OBJ, src + ".o")
-    cmd = [_hipcc(), "-x", "hip", *HIP_FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), "-x", "hip", *HIP_FLAGS, *FILE_FLAGS.get(src, []), *extra, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compiling {src} failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
