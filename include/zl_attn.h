@@ -106,6 +106,9 @@ typedef struct zl_seg_desc {
   int32_t num_slots;           /* partial slots; >= 1 when any SHARD exists       */
 } zl_seg_desc;
 
+/* Largest num_heads any attention entry point accepts. */
+#define ZL_MAX_HEADS 16384
+
 /* ABI version this library was built with (ZL_ABI_VERSION). */
 int32_t zl_abi_version(void);
 
@@ -129,7 +132,9 @@ zl_status zl_workspace_size(const zl_seg_desc* desc, int32_t num_heads, int32_t 
  * q [Tq,H,d], k/v [Tk,H,d] in `dtype` (ZL_BF16; ZL_FP32 for plumbing runs),
  * out [Tq,H,d] in `dtype`, lse [Tq,H] fp32.  out/lse may be NULL when there
  * are no WHOLE rows, o_part/lse_part when there are no SHARD rows.  Rows of
- * other kinds are not written.  head_dim must be 64 or 128.
+ * other kinds are not written.  head_dim must be 64 or 128; num_heads at most
+ * ZL_MAX_HEADS (ZL_ERR_UNSUPPORTED beyond: the kernels address the rows of a
+ * 64-row tile with 32-bit byte offsets from its first row).
  */
 zl_status zl_attn_fwd(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
                       float softmax_scale, const void* q, const void* k, const void* v,

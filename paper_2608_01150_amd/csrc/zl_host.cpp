@@ -161,6 +161,9 @@ zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_
 
 zl_status validate_common(int32_t H, int32_t hd, zl_dtype dt, float scale, bool need_scale) {
   if (H < 1) return fail(ZL_ERR_INVALID_ARG, "num_heads must be >= 1 (got %d)", H);
+  if (H > ZL_MAX_HEADS)
+    return fail(ZL_ERR_UNSUPPORTED, "num_heads %d exceeds %d (tile rows are addressed with 32-bit offsets)", H,
+                ZL_MAX_HEADS);
   if (hd != 64 && hd != 128) return fail(ZL_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", hd);
   if (dt != ZL_BF16 && dt != ZL_FP32) return fail(ZL_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
   if (need_scale && !(std::isfinite(scale) && scale > 0.f))

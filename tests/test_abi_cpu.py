@@ -71,6 +71,8 @@ def test_invalid_descriptors_are_rejected(over, needle):
 def test_invalid_scalars_and_pointers():
     d = _ok_desc()
     assert _fwd(d, H=0) == api.ZL_ERR_INVALID_ARG
+    assert _fwd(d, H=16385) == api.ZL_ERR_UNSUPPORTED  # ZL_MAX_HEADS + 1
+    assert "exceeds 16384" in api.last_error()
     assert _fwd(d, hd=96) == api.ZL_ERR_UNSUPPORTED
     assert _fwd(d, scale=0.0) == api.ZL_ERR_INVALID_ARG
     assert _fwd(d, scale=float("nan")) == api.ZL_ERR_INVALID_ARG
