@@ -22,7 +22,13 @@ pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not HAVE_GPU, reason="needs a 
 H, HD = 16384, 128
 
 
-def test_max_heads_forward_merge_backward():
+@pytest.fixture
+def release_cache():
+    yield
+    torch.cuda.empty_cache()  # about 62 GB of tensors; later tests in the process need none of it
+
+
+def test_max_heads_forward_merge_backward(release_cache):
     d = _descs.desc(cu_q=(0, 1100, 1170, 1210), kind=(0, 0, 1), kv_first=(0, 1, 2), kv_count=(1, 1, 2),
                     cu_k=(0, 1100, 1170, 1220, 1250), block_index=(0, 0, 1, 0), num_slots=2,
                     q_offset=(0, 0, 0), k_offset=(0, 0, 0, 50))
