@@ -4,9 +4,9 @@ TEST INFRASTRUCTURE (see the package docstring).
 
 Sec. IV-D of the paper lowers a placement into a rank-local schedule: each
 rank materialises only its assigned tokens from the sequences' global token
-ranges, orders segments deterministically (decreasing split degree, ties by
-global placement order) and runs every whole sequence in one block-diagonal
-call.  Here a "segment" is what one rank holds of one sequence: a whole
+ranges, sorts its segments deterministically (by split degree, largest
+first, with the global placement settling ties) and runs every whole
+sequence in one block-diagonal call.  Here a "segment" is what one rank holds of one sequence: a whole
 sequence, configuration (1,1,1) in Sec. IV-A, or a local query shard that
 attends to a list of K/V blocks (the ring axis of Tab. II).
 
@@ -19,8 +19,8 @@ and the order the scheduler must emit them in:
     ``block_n`` keys), each item covering all of the segment's query rows.
 Cost of an item = rows x keys (attention work is quadratic, Sec. II-A).  The
 order is cost descending, ties broken by (segment, head, q_start, k_start,
-range index) ascending: the analogue of the paper's "decreasing split degree,
-ties by placement order" rule, applied to work items instead of collectives.
+range index) ascending: the Sec. IV-D segment ordering (largest first, a
+fixed input order settling ties) carried over to work items.
 
 An item is the 8-tuple
   (q_start, q_len, k_start, k_len, head, slot, segment, range)
