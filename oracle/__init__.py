@@ -28,6 +28,7 @@ function here is "parity unpinned".
 from .attention import (  # noqa: F401
     attend,
     attend_bwd,
+    attend_bwd_given,
     lse_merge,
     packed_forward,
     packed_backward,

@@ -149,6 +149,48 @@ def attend_bwd(q, k, v, do, scale, q_rows=None, k_rows=None):
     return dq, dk, dv
 
 
+def attend_bwd_given(q, k, v, do, o, lse, scale, q_rows=None, k_rows=None):
+    """The same gradient formulas with O and LSE supplied by the caller.
+
+    The backward of a CP shard runs on the final (merged) O and LSE of its
+    rows, which another step produced and stored (the backward reading of the
+    design notes); this entry takes them as inputs instead of recomputing
+    them, so a stored (rounded) O or LSE enters exactly where it would:
+      D_i   = dO_i . O_i                (O as given)
+      P_ij  = exp(S_ij - LSE_i)         (LSE as given)
+      dV_j  = sum_i P_ij dO_i
+      dP_ij = dO_i . v_j
+      dS_ij = P_ij (dP_ij - D_i)
+      dQ_i  = scale * sum_j dS_ij k_j
+      dK_j  = scale * sum_i dS_ij q_i
+    q [Lq, d], k, v [Lk, d], do, o [Lq, d], lse [Lq].  With the exact O and
+    LSE of ``attend`` this is ``attend_bwd``.  ``q_rows`` / ``k_rows`` select
+    the returned rows as in ``attend_bwd``.
+    """
+    q, k, v, do, o, lse = _f64(q), _f64(k), _f64(v), _f64(do), _f64(o), _f64(lse)
+    lq, lk = q.shape[0], k.shape[0]
+    qi = np.arange(lq) if q_rows is None else np.asarray(q_rows, np.int64)
+    kj = np.arange(lk) if k_rows is None else np.asarray(k_rows, np.int64)
+    dq = np.zeros((qi.size, k.shape[1]), np.float64)
+    dk = np.zeros((kj.size, q.shape[1]), np.float64)
+    dv = np.zeros((kj.size, do.shape[1]), np.float64)
+    if lq == 0 or lk == 0:
+        return dq, dk, dv
+    dsum = (do * o).sum(axis=1)
+    if qi.size:
+        s = scale * (q[qi] @ k.T)
+        p = np.exp(s - lse[qi, None])
+        ds = p * (do[qi] @ v.T - dsum[qi, None])
+        dq = scale * (ds @ k)
+    if kj.size:
+        s = scale * (q @ k[kj].T)
+        p = np.exp(s - lse[:, None])
+        ds = p * (do @ v[kj].T - dsum[:, None])
+        dv = p.T @ do
+        dk = scale * (ds.T @ q)
+    return dq, dk, dv
+
+
 # ---------------------------------------------------------------------------
 # Packed batches.  A descriptor is any mapping (or object) with the fields
 #   cu_seqlens_q [nq+1], kind [nq] (0 whole, 1 shard), kv_first [nq],
