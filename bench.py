@@ -1,19 +1,24 @@
 """Benchmark of the packed whole+shard attention hot path on one MI355X.
 
 One step = the whole path over one packed batch: one forward launch over the
-WHOLE and SHARD segments together, the LSE merge of the shard partials, and
-the backward (preprocess, dK/dV, dQ), inputs resident in HBM.  The
-default workload is the coalesced whole+shard batch: one GPU's share of a
-75,600-token 720p video at CP=8 (a 9450-query shard against all 8 K/V blocks
-of 9450 tokens) packed with six whole 1560-token images, 40 heads, d=128,
-bf16.  It is the one batch that exercises every step of the path.
+WHOLE and SHARD segments together, the LSE merge of the shard partials (when
+the batch has shards), and the backward (preprocess, dK/dV, dQ), inputs
+resident in HBM.  The default workload is the mixed image-video batch: one
+32,760-token 480p video, two 3600-token and eight 1560-token images, all
+whole, coalesced into one block-diagonal launch (Sec. IV-D), 40 heads, d=128,
+bf16, the video's Q and K scaled by 4.  It has no shards, so the same run also
+times the LSE merge on the coalesced whole+shard batch (one GPU's share of a
+75,600-token video at CP=8: a 9450-query shard's 8 block partials), reported
+as merge_kernel with its own workload name.
 
 Prints one JSON line.  value = fwd+bwd TFLOP/s with the FlashAttention FLOP
 convention (forward 4*d*H*pairs, backward 10*d*H*pairs, pairs = block-diagonal
 query-key pairs only).  roofline = the dominant (longest) kernel, timed with
-HIP events on the stream it is launched on inside the timed region and priced at the MFMA
-FLOPs it executes per pair (forward 4d, dK/dV 8d, dQ 6d) against the bf16
-dense MFMA peak.
+HIP events on the stream it is launched on inside the timed region, priced at
+its share of the algorithmic FLOPs (no recompute: forward S and PV 4*d per
+pair, dK/dV kernel dP, dV, dK 6*d, dQ kernel dQ 2*d; 12*d per step) against
+the bf16 dense MFMA peak; the executed rate (4, 8, 6 *d, recompute included)
+and its fraction of a bf16 GEMM measured in the same run stand beside it.
 cpu_baseline = the fp64 oracle timed on this host's cores on a bounded
 sample of the same batch (see --cpu-seconds).
 """
@@ -35,7 +40,11 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c4", help="c2..c5 (default c4: coalesced whole+shard)")
+    ap.add_argument("--workload", default="c3", help="c2..c5 (default c3: mixed image-video batch)")
+    ap.add_argument("--merge-workload", default="c4",
+                    help="when the workload has no shards: the batch whose LSE merge is timed in the same run")
+    ap.add_argument("--merge-reps", type=int, default=20, help="timed merge launches on --merge-workload")
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the bf16 GEMM ceiling measurement")
     ap.add_argument("--ulysses-group", type=int, default=8, help="group size h for --mode ulysses")
     ap.add_argument("--partials", default="fp32", choices=("fp32", "bf16"),
                     help="--mode blocks: dtype of the shard partials between the forward and the merge "
@@ -57,15 +66,21 @@ def parse():
     return ap.parse_args()
 
 
+# CPU baseline sample: a shard keeps the first 1/SHARD_DIV of its query rows, a whole segment longer
+# than LONG_WHOLE the first 1/LONG_DIV (each against all of its keys).
+LONG_WHOLE, SHARD_DIV, LONG_DIV = 8192, 9, 27
+
+
 def cpu_baseline(w, min_seconds):
     """Time the oracle (as it stands) on a bounded sample of workload w.
 
     Sample: heads taken one at a time until at least `min_seconds` of oracle
     time has accumulated (or every head is done); per head, every whole
-    segment in full (forward + backward) and each shard reduced to its first
-    1/9 of query rows, forward against all of its blocks, merge, backward
-    against all blocks.  FLOPs are counted with the same convention as the
-    GPU value (14*d per pair).
+    segment of up to LONG_WHOLE tokens in full (forward + backward), each
+    shard reduced to its first 1/SHARD_DIV of query rows and each longer
+    whole segment to its first 1/LONG_DIV, forward against all of its keys
+    (blocks), merge, backward.  FLOPs are counted with the same convention as
+    the GPU value (14*d per pair).
     """
     import numpy as np
     import oracle
@@ -78,14 +93,16 @@ def cpu_baseline(w, min_seconds):
         cores = os.cpu_count() or 1
     d = w.desc_dict()
     cq = list(d["cu_seqlens_q"])
-    new_cq, rows = [0], []
+    new_cq, rows, kinds = [0], [], list(d["kind"])
     for s in range(w.num_segments):
         a, b = cq[s], cq[s + 1]
-        if w.kind[s] == W.SHARD:
-            b = a + (b - a + 8) // 9
+        if w.kind[s] == W.SHARD or b - a > LONG_WHOLE:
+            div = SHARD_DIV if w.kind[s] == W.SHARD else LONG_DIV
+            b = a + (b - a + div - 1) // div
+            kinds[s] = W.SHARD   # a query subset against all of the segment's keys
         rows.append((a, b))
         new_cq.append(new_cq[-1] + (b - a))
-    d2 = dict(d, cu_seqlens_q=tuple(new_cq))
+    d2 = dict(d, cu_seqlens_q=tuple(new_cq), kind=tuple(kinds), num_slots=max(1, d["num_slots"]))
     pairs = 0
     for s in range(w.num_segments):
         lq = new_cq[s + 1] - new_cq[s]
@@ -109,8 +126,9 @@ def cpu_baseline(w, min_seconds):
         heads += 1
     flops = 14.0 * w.head_dim * heads * pairs
     return {"value": flops / spent / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{heads} of {w.num_heads} heads; whole segments in full, each shard's first 1/9 of "
-                      f"query rows against all blocks; fwd+merge+bwd fp64; {pairs} pairs/head, {spent:.1f} s"}
+            "sample": f"{heads} of {w.num_heads} heads; whole segments up to {LONG_WHOLE} tokens in full, the first "
+                      f"1/{SHARD_DIV} of each shard's query rows and the first 1/{LONG_DIV} of each longer whole "
+                      f"segment's, against all of their keys; fwd+merge+bwd fp64; {pairs} pairs/head, {spent:.1f} s"}
 
 
 def gathered_descriptor(w):
@@ -227,15 +245,81 @@ def kernel_source_hash(kernel: str) -> str:
 
 def stored_traffic(kernel: str, workload: str):
     """HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE (copy-calibrated)
-    for this kernel and workload, or None if absent or taken on different kernel source."""
+    for this kernel and workload ({kernel: {workload name: record}} in the file), or None if absent
+    or taken on different kernel source."""
     try:
         with open(TRAFFIC_FILE) as fh:
-            rec = json.load(fh).get(kernel)
-    except (OSError, ValueError):
+            rec = json.load(fh).get(kernel, {}).get(workload)
+    except (OSError, ValueError, AttributeError):
         return None
-    if not rec or rec.get("workload") != workload or rec.get("src_sha256") != kernel_source_hash(kernel):
+    if not rec or rec.get("src_sha256") != kernel_source_hash(kernel):
         return None
     return rec
+
+
+def merge_on(name, reps, partials):
+    """Times the LSE merge on workload `name` (one forward fills its partials, then `reps` merge
+    launches); returns the merge_kernel record.  Used when the benchmarked batch has no shards."""
+    import torch
+    from paper_2608_01150_amd import api
+    from paper_2608_01150_amd import workloads as W
+    w = W.get(name)
+    dev = torch.device("cuda:0")
+    desc = api.SegDesc.of(w)
+    H, hd = w.num_heads, w.head_dim
+    q, k, v = (w.full(t, device=dev) for t in (W.TENSOR_Q, W.TENSOR_K, W.TENSOR_V))
+    pdt = torch.bfloat16 if partials == "bf16" else torch.float32
+    out = torch.empty_like(q)
+    lse = torch.empty((w.total_q, H), dtype=torch.float32, device=dev)
+    o_part = torch.empty((w.num_slots, w.total_q, H, hd), dtype=pdt, device=dev)
+    lse_part = torch.empty((w.num_slots, w.total_q, H), dtype=torch.float32, device=dev)
+    api.attn_fwd(desc, q, k, v, w.scale, out, lse, o_part, lse_part)
+    for _ in range(3):
+        api.lse_merge(desc, o_part, lse_part, out, lse)
+    torch.cuda.synchronize()
+    api.profile_reset()
+    api.profile_enable(True)
+    for _ in range(reps):
+        api.lse_merge(desc, o_part, lse_part, out, lse)
+    torch.cuda.synchronize()
+    api.profile_enable(False)
+    ms_total, n = api.profile_read(api.ZL_K_MERGE)
+    rec = merge_record(w, H, hd, partials, ms_total / n)
+    rec.update(workload=w.name, launches=n)
+    del q, k, v, out, lse, o_part, lse_part
+    torch.cuda.empty_cache()
+    return rec
+
+
+def merge_record(w, H, hd, partials, ms):
+    from paper_2608_01150_amd import workloads as W
+    sr = w.shard_rows()
+    nb = max(w.kv_count[s] for s in range(w.num_segments) if w.kind[s] == W.SHARD)
+    pb = 2 if partials == "bf16" else 4   # bytes per partial element
+    mbytes = H * sr * (nb * (pb * hd + 4) + 2 * hd + 4)
+    gbs = mbytes / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": mbytes, "ms": round(ms, 4)}
+
+
+def gemm_ceiling(n=8192, reps=10):
+    """bf16 GEMM rate (torch.matmul, hipBLASLt) on this GPU in this run: a measured ceiling for dense
+    bf16 MFMA work with no attention dependencies."""
+    import torch
+    a = torch.randn((n, n), device="cuda:0").to(torch.bfloat16)
+    b = torch.randn((n, n), device="cuda:0").to(torch.bfloat16)
+    for _ in range(3):
+        c = a @ b
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        c = a @ b
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    del a, b, c
+    return {"kind": f"bf16 GEMM {n}^3 (torch.matmul, hipBLASLt)", "tflops": round(2.0 * n ** 3 / (ms * 1e-3) / 1e12, 1)}
 
 
 def main():
@@ -378,16 +462,33 @@ def main():
         H = H_report            # this GPU computes H/h heads of every sequence
     fa_flops = 14.0 * hd * H * pairs
     value = fa_flops / (ms * 1e-3) / 1e12
-    # MFMA FLOPs each kernel executes per block-diagonal pair (x d x H):
-    # forward S and PV (4); dK/dV kernel S, dP, dV, dK (8); dQ kernel S, dP, dQ (6).
-    per_pair = {"fwd": 4.0, "bwd_dkdv": 8.0, "bwd_dq": 6.0}
+    # MFMA FLOPs per block-diagonal pair (x d x H) each kernel executes (forward S and PV: 4; dK/dV
+    # kernel S, dP, dV, dK: 8; dQ kernel S, dP, dQ: 6) and its share of the algorithmic 12 per step
+    # (no recompute: the forward's 4, dP, dV and dK of the dK/dV kernel, dQ of the dQ kernel).
+    executed = {"fwd": 4.0, "bwd_dkdv": 8.0, "bwd_dq": 6.0}
+    algorithmic = {"fwd": 4.0, "bwd_dkdv": 6.0, "bwd_dq": 2.0}
+    ceiling = None if args.no_ceiling else gemm_ceiling()
     kern = {}
-    for name, f in per_pair.items():
+    for name, f in executed.items():
         if avg.get(name):
-            t = f * hd * H * pairs / (avg[name] * 1e-3) / 1e12
-            kern[name] = {"ms": round(avg[name], 4), "tflops": round(t, 2), "frac": round(t / BF16_PEAK_TFLOPS, 4),
-                          "flops_per_pair_per_d": f}
+            per_s = hd * H * pairs / (avg[name] * 1e-3) / 1e12
+            kern[name] = {"ms": round(avg[name], 4),
+                          "algorithmic_tflops": round(algorithmic[name] * per_s, 2),
+                          "frac": round(algorithmic[name] * per_s / BF16_PEAK_TFLOPS, 4),
+                          "executed_tflops": round(f * per_s, 2),
+                          "frac_executed": round(f * per_s / BF16_PEAK_TFLOPS, 4),
+                          "flops_per_pair_per_d": {"algorithmic": algorithmic[name], "executed": f}}
     dom = max(kern, key=lambda n: kern[n]["ms"])
+    alg12 = 12.0 * hd * H * pairs / (ms * 1e-3) / 1e12
+    roof = {"bound": "mfma", "kernel": dom, "achieved": kern[dom]["algorithmic_tflops"], "peak": BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": kern[dom]["frac"], "traffic": None,
+            "flops_per_pair_per_d": algorithmic[dom],
+            "executed_tflops": kern[dom]["executed_tflops"], "frac_executed": kern[dom]["frac_executed"],
+            "step_frac_algorithmic_12d": round(alg12 / BF16_PEAK_TFLOPS, 4),
+            "step_frac_fa_14d": round(value / BF16_PEAK_TFLOPS, 4)}
+    if ceiling:
+        roof["measured_ceiling"] = ceiling
+        roof["frac_executed_of_measured_ceiling"] = round(kern[dom]["executed_tflops"] / ceiling["tflops"], 4)
     rec = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
@@ -396,11 +497,10 @@ def main():
                    "total_k": w.total_k,
                    "pairs_per_head": pairs, "shard_rows": w.shard_rows(), "num_slots": w.num_slots},
         "pct_of_mfma_peak": round(100.0 * value / BF16_PEAK_TFLOPS, 2),
-        "algorithmic_tflops_12d": round(12.0 * hd * H * pairs / (ms * 1e-3) / 1e12, 2),
+        "algorithmic_tflops_12d": round(alg12, 2),
         "kernel_ms": {n: round(a, 4) for n, a in avg.items()},
         "kernels": kern,
-        "roofline": {"bound": "mfma", "kernel": dom, "achieved": kern[dom]["tflops"], "peak": BF16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": kern[dom]["frac"], "traffic": None},
+        "roofline": roof,
     }
     tr = stored_traffic(dom, w.name)
     if tr:
@@ -408,13 +508,10 @@ def main():
         rec["roofline"]["traffic_detail"] = {"fetch_bytes": tr["fetch_bytes"], "write_bytes": tr["write_bytes"],
                                              "unique_input_output_bytes": tr.get("unique_bytes")}
     if w.num_slots and avg.get("merge"):
-        sr = w.shard_rows()
-        nb = max(w.kv_count[s] for s in range(w.num_segments) if w.kind[s] == W.SHARD)
-        pb = 2 if args.partials == "bf16" else 4   # bytes per partial element
-        mbytes = H * sr * (nb * (pb * hd + 4) + 2 * hd + 4)
-        gbs = mbytes / (avg["merge"] * 1e-3) / 1e9
-        rec["merge_kernel"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                               "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": mbytes}
+        rec["merge_kernel"] = merge_record(w, H, hd, args.partials, avg["merge"])
+        rec["merge_kernel"]["workload"] = w.name
+    elif args.mode == "blocks" and args.merge_reps > 0:
+        rec["merge_kernel"] = merge_on(args.merge_workload, args.merge_reps, args.partials)
     # Host scheduler: building the forward, dK/dV and dQ work tables of this batch (what the cached
     # plan saves on every later call; zl_plan_dump runs the same builder on the host).
     t0 = time.perf_counter()

@@ -30,12 +30,15 @@
  *     zl_last_error() then describes the problem.  No C++ exception crosses
  *     this boundary.
  *   - The library owns one cache of device work tables (the schedule of a
- *     descriptor), created on the first call with a new descriptor, reused
- *     afterwards and released by zl_shutdown().  It allocates no other
- *     device memory.  Once a descriptor's tables exist, calls with it only
- *     launch kernels (no allocation, copy, memset or synchronisation), so
- *     they may be captured in a HIP graph; make the first call eagerly, and
- *     keep profiling off while capturing.
+ *     descriptor), created on the first call with a new descriptor (which
+ *     allocates the table and uploads it on the call's stream), reused
+ *     afterwards and kept until zl_shutdown(): no call frees a table, so a
+ *     table's address stays valid for every graph that captured it, and no
+ *     call synchronises the device.  A table takes 32 bytes per work item.
+ *     The library allocates no other device memory.  Once a descriptor's
+ *     tables exist, calls with it only launch kernels (no allocation, copy,
+ *     memset or synchronisation), so they may be captured in a HIP graph;
+ *     make the first call eagerly, and keep profiling off while capturing.
  */
 #ifndef ZL_ATTN_H
 #define ZL_ATTN_H
@@ -177,7 +180,8 @@ zl_status zl_attn_fwd_ex(const zl_seg_desc* desc, int32_t num_heads, int32_t hea
  * packed query row like out/lse; only SHARD rows are read or written, and
  * they may be NULL when there are no SHARD rows or when flags is
  * ZL_STEP_FIRST|ZL_STEP_LAST.  Without ZL_STEP_FIRST they must hold the
- * previous step's result.  block_index and num_slots are not used.  Calls
+ * previous step's result.  block_index and num_slots are not read (any
+ * values, block_index may be NULL).  Calls
  * for different steps must be ordered on the stream (the accumulator is
  * read-modify-written).  Errors as zl_attn_fwd, plus ZL_ERR_INVALID_ARG for
  * a SHARD segment with kv_count != 1 or unknown flags.
@@ -255,8 +259,10 @@ zl_status zl_lse_merge_ex(const zl_seg_desc* desc, int32_t num_heads, int32_t he
  *   dk_j = scale sum_i dS_ij q_i,  dv_j = sum_i P_ij dO_i
  * (for a SHARD block: this query chunk's contribution).  All tensors in
  * `dtype` (ZL_BF16 only) except lse (fp32).  dq is [Tq,H,d] and every row of
- * it is written; dk, dv are [Tk,H,d] and rows of ranges no segment uses are
- * not written.  No atomics: results are deterministic.  `flags` must be 0.
+ * it is written; dk, dv are [Tk,H,d]: every row of a range that a segment
+ * uses is written (zeros for the ranges of a SHARD segment without query
+ * rows, to which no query attends), rows of ranges no segment uses are not.
+ * No atomics: results are deterministic.  `flags` must be 0.
  * workspace: at least zl_workspace_size(..., ZL_OP_BWD) bytes of device
  * memory, 256-byte aligned, used by this call until it completes.
  */
@@ -364,7 +370,8 @@ zl_status zl_profile_read(int32_t kernel_id, double* total_ms, int64_t* launches
 void zl_profile_reset(void);
 
 /* Releases the library's device work-table cache and any pending profiler
- * events (waits for the device). */
+ * events (waits for the device first, so no enqueued kernel still reads a
+ * table).  Graphs that captured library calls must not be replayed after it. */
 void zl_shutdown(void);
 
 #ifdef __cplusplus

@@ -16,7 +16,8 @@ and the order the scheduler must emit them in:
   * forward: one item per (segment, head, query tile of ``block_m`` rows,
     K/V range of the segment);
   * backward: one item per (segment, head, K/V range, key tile of
-    ``block_n`` keys), each item covering all of the segment's query rows.
+    ``block_n`` keys), each item covering all of the segment's query rows
+    (none, for a shard without query rows: its keys' gradient is zero).
 Cost of an item = rows x keys (attention work is quadratic, Sec. II-A).  The
 order is cost descending, ties broken by (segment, head, q_start, k_start,
 range index) ascending: the Sec. IV-D segment ordering (largest first, a
@@ -77,7 +78,10 @@ def work_items(desc, num_heads, op, block_m, block_n):
     for s in range(len(kinds)):
         q0, q1 = int(cq[s]), int(cq[s + 1])
         lq = q1 - q0
-        if lq == 0:
+        # A segment without query rows has no forward or dQ work; its ranges
+        # still get key-tile items, since their dK/dV (zero: no query attends
+        # to them) is part of the backward's output.
+        if lq == 0 and op != 1:
             continue
         shard = int(kinds[s]) == SHARD
         if op == 2:

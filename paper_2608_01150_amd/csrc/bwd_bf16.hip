@@ -568,6 +568,7 @@ hipError_t launch_bwd_bf16(const BwdParams& p, int head_dim, int stage, hipStrea
   const dim3 block(NT);
   if (stage == 0) {
     const int64_t units = p.total_q * p.num_heads;
+    if (units == 0) return hipSuccess;
     const int upb = NT / (head_dim / 8);
     const dim3 grid((unsigned)((units + upb - 1) / upb));
     if (head_dim == 128) hipLaunchKernelGGL(bwd_pre_kernel<128>, grid, block, 0, s, p);

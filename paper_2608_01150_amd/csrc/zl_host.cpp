@@ -4,12 +4,13 @@
 // The scheduler lowers a rank-local segment list (Sec. IV-D of arXiv
 // 2608.01150: the placement materialised as the rank's own token ranges) into
 // work items and orders them longest-processing-time first: cost = rows x keys,
-// the quadratic attention work of Sec. II-A.  Ties follow segment order, the
-// analogue of the engine's "decreasing split degree, ties by placement order"
-// rule.  With the hardware dispatcher handing each free compute unit the next
-// workgroup in this order, the launch runs as greedy list scheduling of the
-// items in LPT order, the same "largest first, to the least-loaded place"
-// rule the paper's Filler Packing (Eq. 8) uses across ranks.
+// the quadratic attention work of Sec. II-A.  Ties follow segment order, as
+// Sec. IV-D sorts a rank's segments by split degree with a fixed placement
+// order settling ties.  With the hardware dispatcher handing each free compute
+// unit the next workgroup in this order, the launch runs as greedy list
+// scheduling of the items in LPT order: each item goes, largest first, to the
+// least-loaded place, as the paper's Filler Packing (Eq. 8) places fillers
+// across ranks.
 
 #include "zl_attn.h"
 #include "zl_internal.h"
@@ -20,7 +21,6 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
-#include <list>
 #include <mutex>
 #include <string>
 #include <unordered_map>
@@ -193,16 +193,22 @@ TileCfg tile_cfg(zl_dtype dt, int op) {
 }
 
 // Internal plan kinds beside the public ZL_OP_* codes: the merge table, and
-// the backward of a ring step, whose dQ items mark SHARD rows (slot 0).
+// the forward and backward of a ring step.  Step plans ignore block_index:
+// their SHARD items carry slot 0, which only marks them as SHARD.
 constexpr int kPlanMerge = 2;
 constexpr int kPlanBwdStep = 5;
+constexpr int kPlanFwdStep = 6;
 
-// mark_shard: dQ items of SHARD segments carry slot 0 instead of -1.
-std::vector<zl::Item> build_items(const zl_seg_desc* d, int32_t H, int op, TileCfg t, bool mark_shard = false) {
+bool is_step_plan(int op) { return op == kPlanFwdStep || op == kPlanBwdStep; }
+
+// step: SHARD items carry slot 0 instead of their block's slot (dQ items:
+// instead of -1).  dK/dV items also cover the ranges of a SHARD segment with
+// no query rows: their gradient is zero, and the kernel stores it.
+std::vector<zl::Item> build_items(const zl_seg_desc* d, int32_t H, int op, TileCfg t, bool step = false) {
   std::vector<zl::Item> items;
   for (int32_t s = 0; s < d->num_q_segs; ++s) {
     const int32_t q0 = d->cu_seqlens_q[s], q1 = d->cu_seqlens_q[s + 1];
-    if (q1 == q0) continue;
+    if (q1 == q0 && op != ZL_OP_BWD) continue;
     const bool shard = d->kind[s] == ZL_SHARD;
     if (op == ZL_OP_BWD_DQ) {
       const int32_t j0 = d->kv_first[s], j1 = j0 + d->kv_count[s];
@@ -210,13 +216,12 @@ std::vector<zl::Item> build_items(const zl_seg_desc* d, int32_t H, int op, TileC
       const int32_t total = d->cu_seqlens_k[j1] - d->cu_seqlens_k[j0];
       for (int32_t h = 0; h < H; ++h)
         for (int32_t t0 = q0; t0 < q1; t0 += t.m)
-          items.push_back({t0, std::min(t.m, q1 - t0), d->cu_seqlens_k[j0], total, h, mark_shard && shard ? 0 : -1, s,
-                           j0});
+          items.push_back({t0, std::min(t.m, q1 - t0), d->cu_seqlens_k[j0], total, h, step && shard ? 0 : -1, s, j0});
       continue;
     }
     for (int32_t j = d->kv_first[s]; j < d->kv_first[s] + d->kv_count[s]; ++j) {
       const int32_t k0 = d->cu_seqlens_k[j], k1 = d->cu_seqlens_k[j + 1];
-      const int32_t slot = shard ? (d->block_index ? d->block_index[j] : 0) : -1;  // ring step: slot unused, >= 0 marks SHARD
+      const int32_t slot = shard ? (step ? 0 : d->block_index[j]) : -1;
       for (int32_t h = 0; h < H; ++h) {
         if (op == ZL_OP_FWD) {
           for (int32_t t0 = q0; t0 < q1; t0 += t.m)
@@ -263,7 +268,6 @@ MergeTable build_merge(const zl_seg_desc* d, int32_t H) {
 // ------------------------------------------------------------- plan cache
 
 struct Plan {
-  std::vector<int64_t> key;
   int device = -1;
   void* dev = nullptr;          // device copy of the table(s)
   std::vector<char> host;       // host copy (source of the upload)
@@ -276,9 +280,27 @@ struct Plan {
 
 size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
+// Bytes of the backward's D and LSE*log2(e) workspace: two fp32 [Tq, H] arrays.
+size_t bwd_workspace_bytes(const Shape& sh, int32_t H) { return 2 * align256((size_t)sh.total_q * H * sizeof(float)); }
+
+struct KeyHash {
+  size_t operator()(const std::vector<int64_t>& k) const noexcept {
+    uint64_t h = 1469598103934665603ull;  // FNV-1a over the 64-bit words
+    for (int64_t x : k) {
+      h ^= (uint64_t)x;
+      h *= 1099511628211ull;
+    }
+    return (size_t)h;
+  }
+};
+
+// Every table stays cached until zl_shutdown: a call never frees one, so a
+// HIP graph captured after a descriptor's first call keeps valid table
+// addresses, and no call has to synchronise the device to retire a table.
+// A table is 32 bytes per work item (under 6 MB for the largest batches
+// here).  Node-based, so Plan pointers stay valid as the map grows.
 std::mutex g_mu;
-std::list<Plan> g_plans;  // most recently used first
-constexpr size_t kMaxPlans = 64;
+std::unordered_map<std::vector<int64_t>, Plan, KeyHash> g_plans;
 
 std::vector<int64_t> plan_key(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int op, int dev) {
   std::vector<int64_t> k = {op, (int64_t)dt, H, hd, dev, d->num_q_segs, d->num_kv_ranges, d->num_slots};
@@ -289,29 +311,15 @@ std::vector<int64_t> plan_key(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dt
     k.push_back(d->kv_count[s]);
   }
   for (int32_t j = 0; j <= d->num_kv_ranges; ++j) k.push_back(d->cu_seqlens_k[j]);
-  for (int32_t j = 0; j < d->num_kv_ranges; ++j) k.push_back(d->block_index ? d->block_index[j] : 0);
+  const bool slots = !is_step_plan(op) && d->block_index;  // step plans do not read block_index
+  for (int32_t j = 0; j < d->num_kv_ranges; ++j) k.push_back(slots ? d->block_index[j] : 0);
   return k;
 }
 
-zl_status insert_plan(Plan&& p, hipStream_t stream, Plan** out);
+zl_status insert_plan(std::vector<int64_t>&& key, Plan&& p, hipStream_t stream, Plan** out);
 
-// Returns the cached plan for this descriptor, building and uploading it on a
-// miss.  Caller holds g_mu.
-zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int op, hipStream_t stream,
-                   Plan** out) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return fail(ZL_ERR_HIP, "hipGetDevice failed: no usable GPU");
-  std::vector<int64_t> key = plan_key(d, H, hd, dt, op, dev);
-  for (auto it = g_plans.begin(); it != g_plans.end(); ++it) {
-    if (it->key == key) {
-      g_plans.splice(g_plans.begin(), g_plans, it);
-      *out = &g_plans.front();
-      return ZL_OK;
-    }
-  }
-  Plan p;
-  p.key = std::move(key);
-  p.device = dev;
+// Builds the host copy of a plan's table(s) into p.
+zl_status build_plan_host(const zl_seg_desc* d, int32_t H, zl_dtype dt, int op, Plan& p) {
   if (op == kPlanMerge) {
     MergeTable t = build_merge(d, H);
     p.n_segs = (int32_t)t.segs.size();
@@ -322,8 +330,9 @@ zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int
     if (seg_bytes) std::memcpy(p.host.data(), t.segs.data(), seg_bytes);
     if (!t.slots.empty()) std::memcpy(p.host.data() + p.slots_offset, t.slots.data(), t.slots.size() * 4);
   } else if (op == ZL_OP_BWD || op == kPlanBwdStep) {
-    std::vector<zl::Item> kv = build_items(d, H, ZL_OP_BWD, tile_cfg(dt, ZL_OP_BWD));
-    std::vector<zl::Item> qi = build_items(d, H, ZL_OP_BWD_DQ, tile_cfg(dt, ZL_OP_BWD_DQ), op == kPlanBwdStep);
+    const bool step = op == kPlanBwdStep;
+    std::vector<zl::Item> kv = build_items(d, H, ZL_OP_BWD, tile_cfg(dt, ZL_OP_BWD), step);
+    std::vector<zl::Item> qi = build_items(d, H, ZL_OP_BWD_DQ, tile_cfg(dt, ZL_OP_BWD_DQ), step);
     if (kv.size() > (size_t)INT32_MAX || qi.size() > (size_t)INT32_MAX)
       return fail(ZL_ERR_UNSUPPORTED, "too many work items");
     p.n_items = (int32_t)kv.size();
@@ -333,18 +342,40 @@ zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int
     if (!kv.empty()) std::memcpy(p.host.data(), kv.data(), kv.size() * sizeof(zl::Item));
     if (!qi.empty()) std::memcpy(p.host.data() + p.slots_offset, qi.data(), qi.size() * sizeof(zl::Item));
   } else {
-    std::vector<zl::Item> items = build_items(d, H, op, tile_cfg(dt, op));
+    const bool step = op == kPlanFwdStep;
+    const int base_op = step ? ZL_OP_FWD : op;
+    std::vector<zl::Item> items = build_items(d, H, base_op, tile_cfg(dt, base_op), step);
     if (items.size() > (size_t)INT32_MAX) return fail(ZL_ERR_UNSUPPORTED, "too many work items");
     p.n_items = (int32_t)items.size();
     p.host.resize(items.size() * sizeof(zl::Item));
     if (!items.empty()) std::memcpy(p.host.data(), items.data(), p.host.size());
   }
-  return insert_plan(std::move(p), stream, out);
+  return ZL_OK;
 }
 
-// Uploads a built plan and caches it (most recent first, evicting the oldest
-// beyond kMaxPlans).  Caller holds g_mu.
-zl_status insert_plan(Plan&& p, hipStream_t stream, Plan** out) {
+// Returns the cached plan for this descriptor, building and uploading it on a
+// miss.  Caller holds g_mu.
+zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int op, hipStream_t stream,
+                   Plan** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(ZL_ERR_HIP, "hipGetDevice failed: no usable GPU");
+  std::vector<int64_t> key = plan_key(d, H, hd, dt, op, dev);
+  auto hit = g_plans.find(key);
+  if (hit != g_plans.end()) {
+    *out = &hit->second;
+    return ZL_OK;
+  }
+  Plan p;
+  p.device = dev;
+  zl_status st = build_plan_host(d, H, dt, op, p);
+  if (st != ZL_OK) return st;
+  return insert_plan(std::move(key), std::move(p), stream, out);
+}
+
+
+// Uploads a built plan (stream-ordered, from its own host copy, which the
+// cache keeps alive) and caches it.  Caller holds g_mu.
+zl_status insert_plan(std::vector<int64_t>&& key, Plan&& p, hipStream_t stream, Plan** out) {
   if (!p.host.empty()) {
     if (hipMalloc(&p.dev, p.host.size()) != hipSuccess)
       return fail(ZL_ERR_HIP, "hipMalloc of a %zu-byte work table failed", p.host.size());
@@ -353,20 +384,8 @@ zl_status insert_plan(Plan&& p, hipStream_t stream, Plan** out) {
       return fail(ZL_ERR_HIP, "upload of the work table failed");
     }
   }
-  g_plans.push_front(std::move(p));
-  while (g_plans.size() > kMaxPlans) {
-    Plan& victim = g_plans.back();
-    if (victim.dev) {
-      int cur = 0;
-      (void)hipGetDevice(&cur);
-      (void)hipSetDevice(victim.device);
-      (void)hipDeviceSynchronize();
-      (void)hipFree(victim.dev);
-      (void)hipSetDevice(cur);
-    }
-    g_plans.pop_back();
-  }
-  *out = &g_plans.front();
+  auto ins = g_plans.emplace(std::move(key), std::move(p));
+  *out = &ins.first->second;
   return ZL_OK;
 }
 
@@ -385,12 +404,10 @@ zl_status get_rowmap(int32_t group, int32_t nseq, const int32_t* cu_rank, hipStr
   int64_t total = 0;
   for (int32_t j = 0; j < group; ++j) total += cu_rank[j * w + nseq];
   *total_rows = total;
-  for (auto it = g_plans.begin(); it != g_plans.end(); ++it) {
-    if (it->key == key) {
-      g_plans.splice(g_plans.begin(), g_plans, it);
-      *out = &g_plans.front();
-      return ZL_OK;
-    }
+  auto hit = g_plans.find(key);
+  if (hit != g_plans.end()) {
+    *out = &hit->second;
+    return ZL_OK;
   }
   // full-layout start of each sequence and of each rank's shard inside it
   std::vector<int64_t> seq_start(nseq + 1, 0);
@@ -400,7 +417,6 @@ zl_status get_rowmap(int32_t group, int32_t nseq, const int32_t* cu_rank, hipStr
     seq_start[s + 1] = seq_start[s] + len;
   }
   Plan p;
-  p.key = std::move(key);
   p.device = dev;
   p.host.resize((size_t)total * sizeof(int32_t));
   int32_t* map = reinterpret_cast<int32_t*>(p.host.data());
@@ -413,7 +429,7 @@ zl_status get_rowmap(int32_t group, int32_t nseq, const int32_t* cu_rank, hipStr
       before[s] += n;
     }
   }
-  return insert_plan(std::move(p), stream, out);
+  return insert_plan(std::move(key), std::move(p), stream, out);
 }
 
 zl_status validate_ulysses(int32_t group, int32_t H, int32_t hd, zl_dtype dt) {
@@ -512,7 +528,7 @@ zl_status zl_workspace_size(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_d
     return ok();
   }
   if (op != ZL_OP_BWD) return fail(ZL_ERR_INVALID_ARG, "op must be ZL_OP_FWD or ZL_OP_BWD");
-  *bytes = 2 * align256((size_t)sh.total_q * H * sizeof(float));
+  *bytes = bwd_workspace_bytes(sh, H);
   return ok();
 }
 
@@ -593,7 +609,7 @@ zl_status zl_attn_fwd_step(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dt
   std::lock_guard<std::mutex> lock(g_mu);
   Plan* plan = nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = get_plan(desc, H, hd, dt, ZL_OP_FWD, s, &plan)) != ZL_OK) return st;
+  if ((st = get_plan(desc, H, hd, dt, kPlanFwdStep, s, &plan)) != ZL_OK) return st;
   if (plan->n_items == 0) return ok();
   zl::FwdParams p{};
   p.q = q;
@@ -755,72 +771,102 @@ zl_status zl_lse_merge_ex(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dty
 
 namespace {
 
-// Shared by zl_attn_bwd (step = false) and zl_attn_bwd_step.
-zl_status attn_bwd_impl(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
-                        const void* k, const void* v, const void* out, const float* lse, const void* dout, void* dq,
-                        void* dk, void* dv, bool step, float* dq_acc, uint32_t flags, void* workspace,
-                        size_t ws_bytes, void* stream) {
-  zl_status st = validate_common(H, hd, dt, scale, true);
+// Arguments of one backward call.
+struct BwdCall {
+  const zl_seg_desc* desc;
+  int32_t H, hd;
+  zl_dtype dt;
+  float scale;
+  const void *q, *k, *v, *out;
+  const float* lse;
+  const void* dout;
+  void *dq, *dk, *dv;
+  bool step;        // zl_attn_bwd_step
+  float* dq_acc;
+  uint32_t flags;
+};
+
+// Everything about a backward call except its workspace; fills *sh.
+zl_status validate_bwd(const BwdCall& c, Shape* sh) {
+  zl_status st = validate_common(c.H, c.hd, c.dt, c.scale, true);
   if (st != ZL_OK) return st;
-  if (dt != ZL_BF16) return fail(ZL_ERR_UNSUPPORTED, "backward supports ZL_BF16 only");
-  if (!step && flags != 0) return fail(ZL_ERR_INVALID_ARG, "flags must be 0");
-  if (step && (flags & ~(uint32_t)(ZL_STEP_FIRST | ZL_STEP_LAST)))
+  if (c.dt != ZL_BF16) return fail(ZL_ERR_UNSUPPORTED, "backward supports ZL_BF16 only");
+  if (!c.step && c.flags != 0) return fail(ZL_ERR_INVALID_ARG, "flags must be 0");
+  if (c.step && (c.flags & ~(uint32_t)(ZL_STEP_FIRST | ZL_STEP_LAST)))
     return fail(ZL_ERR_INVALID_ARG, "flags may only hold ZL_STEP_FIRST and ZL_STEP_LAST");
-  const bool first = !step || (flags & ZL_STEP_FIRST), last = !step || (flags & ZL_STEP_LAST);
-  Shape sh;
-  if ((st = validate_desc(desc, 0, false, &sh, step)) != ZL_OK) return st;
-  if ((st = check_sizes(sh, H, hd, 0)) != ZL_OK) return st;
-  if (!sh.ranges_single_owner)
+  const bool first = !c.step || (c.flags & ZL_STEP_FIRST), last = !c.step || (c.flags & ZL_STEP_LAST);
+  if ((st = validate_desc(c.desc, 0, false, sh, c.step)) != ZL_OK) return st;
+  if ((st = check_sizes(*sh, c.H, c.hd, 0)) != ZL_OK) return st;
+  if (!sh->ranges_single_owner)
     return fail(ZL_ERR_INVALID_ARG, "backward needs every K/V range used by at most one segment");
-  if (sh.total_q > 0 && (!q || !out || !lse || !dout || !dq))
+  if (sh->total_q > 0 && (!c.q || !c.out || !c.lse || !c.dout || !c.dq))
     return fail(ZL_ERR_INVALID_ARG, "q, out, lse, dout and dq must not be NULL");
-  if (sh.total_k > 0 && (!k || !v || !dk || !dv)) return fail(ZL_ERR_INVALID_ARG, "k, v, dk and dv must not be NULL");
-  if (step && sh.any_shard_rows && !(first && last) && !dq_acc)
+  if (sh->total_k > 0 && (!c.k || !c.v || !c.dk || !c.dv))
+    return fail(ZL_ERR_INVALID_ARG, "k, v, dk and dv must not be NULL");
+  if (c.step && sh->any_shard_rows && !(first && last) && !c.dq_acc)
     return fail(ZL_ERR_INVALID_ARG, "dq_acc is needed unless flags = ZL_STEP_FIRST | ZL_STEP_LAST");
-  for (const void* p : {q, k, v, out, dout, (const void*)dq, (const void*)dk, (const void*)dv})
+  for (const void* p : {c.q, c.k, c.v, c.out, c.dout, (const void*)c.dq, (const void*)c.dk, (const void*)c.dv})
     if (p && !aligned(p, 16)) return fail(ZL_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
-  if (dq_acc && !aligned(dq_acc, 16)) return fail(ZL_ERR_INVALID_ARG, "dq_acc must be 16-byte aligned");
-  if (lse && !aligned(lse, 4)) return fail(ZL_ERR_INVALID_ARG, "lse must be 4-byte aligned");
-  size_t need = 0;
-  if ((st = zl_workspace_size(desc, H, hd, dt, ZL_OP_BWD, &need)) != ZL_OK) return st;
-  if (need > 0 && (!workspace || ws_bytes < need))
-    return fail(ZL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace ? ws_bytes : 0);
-  if (workspace && !aligned(workspace, 256)) return fail(ZL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-  if (sh.total_q == 0) return ok();
-  std::lock_guard<std::mutex> lock(g_mu);
-  Plan* plan = nullptr;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = get_plan(desc, H, hd, dt, step ? kPlanBwdStep : ZL_OP_BWD, s, &plan)) != ZL_OK) return st;
+  if (c.dq_acc && !aligned(c.dq_acc, 16)) return fail(ZL_ERR_INVALID_ARG, "dq_acc must be 16-byte aligned");
+  if (c.lse && !aligned(c.lse, 4)) return fail(ZL_ERR_INVALID_ARG, "lse must be 4-byte aligned");
+  return ZL_OK;
+}
+
+
+// Enqueues the three backward kernels.  tables: the dK/dV items, then (at
+// q_offset bytes) the dQ items; workspace: bwd_workspace_bytes of device
+// memory.  No early return for Tq = 0: the ranges of a SHARD without query
+// rows still get their (zero) dK/dV.
+zl_status launch_bwd(const BwdCall& c, const Shape& sh, const void* tables, size_t q_offset, int32_t n_kv,
+                     int32_t n_q, void* workspace, hipStream_t s) {
+  const bool first = !c.step || (c.flags & ZL_STEP_FIRST), last = !c.step || (c.flags & ZL_STEP_LAST);
   zl::BwdParams p{};
-  p.q = q;
-  p.k = k;
-  p.v = v;
-  p.out = out;
-  p.lse = lse;
-  p.dout = dout;
-  p.dq = dq;
-  p.dk = dk;
-  p.dv = dv;
+  p.q = c.q;
+  p.k = c.k;
+  p.v = c.v;
+  p.out = c.out;
+  p.lse = c.lse;
+  p.dout = c.dout;
+  p.dq = c.dq;
+  p.dk = c.dk;
+  p.dv = c.dv;
   p.dsum = static_cast<float*>(workspace);
-  p.lse2 = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256((size_t)sh.total_q * H * sizeof(float)));
-  const char* base = static_cast<const char*>(plan->dev);
+  p.lse2 = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256((size_t)sh.total_q * c.H * sizeof(float)));
+  const char* base = static_cast<const char*>(tables);
   p.kv_items = reinterpret_cast<const zl::Item*>(base);
-  p.n_kv_items = plan->n_items;
-  p.q_items = reinterpret_cast<const zl::Item*>(base + plan->slots_offset);
-  p.n_q_items = plan->n_items2;
-  p.num_heads = H;
+  p.n_kv_items = n_kv;
+  p.q_items = reinterpret_cast<const zl::Item*>(base + q_offset);
+  p.n_q_items = n_q;
+  p.num_heads = c.H;
   p.total_q = sh.total_q;
-  p.scale = scale;
-  p.scale_log2 = scale * 1.4426950408889634f;
+  p.scale = c.scale;
+  p.scale_log2 = c.scale * 1.4426950408889634f;
   p.xcd_chunk = xcd_chunk();
-  p.step_mode = step && !(first && last) ? 1 : 0;
+  p.step_mode = c.step && !(first && last) ? 1 : 0;
   p.step_first = first ? 1 : 0;
   p.step_last = last ? 1 : 0;
-  p.dq_acc = dq_acc;
+  p.dq_acc = c.dq_acc;
+  const int hd = c.hd;
   hipError_t e = timed(ZL_K_BWD_PRE, s, [&] { return zl::launch_bwd_bf16(p, hd, 0, s); });
   if (e == hipSuccess) e = timed(ZL_K_BWD_DKDV, s, [&] { return zl::launch_bwd_bf16(p, hd, 1, s); });
   if (e == hipSuccess) e = timed(ZL_K_BWD_DQ, s, [&] { return zl::launch_bwd_bf16(p, hd, 2, s); });
   return hip_status(e, "backward launch");
+}
+
+// Shared by zl_attn_bwd (step = false) and zl_attn_bwd_step.
+zl_status attn_bwd_impl(const BwdCall& c, void* workspace, size_t ws_bytes, void* stream) {
+  Shape sh;
+  zl_status st = validate_bwd(c, &sh);
+  if (st != ZL_OK) return st;
+  const size_t need = bwd_workspace_bytes(sh, c.H);
+  if (need > 0 && (!workspace || ws_bytes < need))
+    return fail(ZL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace ? ws_bytes : 0);
+  if (workspace && !aligned(workspace, 256)) return fail(ZL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  std::lock_guard<std::mutex> lock(g_mu);
+  Plan* plan = nullptr;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = get_plan(c.desc, c.H, c.hd, c.dt, c.step ? kPlanBwdStep : ZL_OP_BWD, s, &plan)) != ZL_OK) return st;
+  return launch_bwd(c, sh, plan->dev, plan->slots_offset, plan->n_items, plan->n_items2, workspace, s);
 }
 
 }  // namespace
@@ -830,16 +876,16 @@ extern "C" {
 zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
                       const void* k, const void* v, const void* out, const float* lse, const void* dout, void* dq,
                       void* dk, void* dv, uint32_t flags, void* workspace, size_t ws_bytes, void* stream) {
-  return attn_bwd_impl(desc, H, hd, dt, scale, q, k, v, out, lse, dout, dq, dk, dv, false, nullptr, flags, workspace,
-                       ws_bytes, stream);
+  const BwdCall c{desc, H, hd, dt, scale, q, k, v, out, lse, dout, dq, dk, dv, false, nullptr, flags};
+  return attn_bwd_impl(c, workspace, ws_bytes, stream);
 }
 
 zl_status zl_attn_bwd_step(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
                            const void* k, const void* v, const void* out, const float* lse, const void* dout, void* dq,
                            void* dk, void* dv, float* dq_acc, uint32_t flags, void* workspace, size_t ws_bytes,
                            void* stream) {
-  return attn_bwd_impl(desc, H, hd, dt, scale, q, k, v, out, lse, dout, dq, dk, dv, true, dq_acc, flags, workspace,
-                       ws_bytes, stream);
+  const BwdCall c{desc, H, hd, dt, scale, q, k, v, out, lse, dout, dq, dk, dv, true, dq_acc, flags};
+  return attn_bwd_impl(c, workspace, ws_bytes, stream);
 }
 
 zl_status zl_plan_dump(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, int32_t op, int32_t* items,
@@ -912,7 +958,8 @@ void zl_shutdown(void) {
   std::lock_guard<std::mutex> lock(g_mu);
   int cur = 0;
   const bool have_dev = hipGetDevice(&cur) == hipSuccess;
-  for (Plan& p : g_plans) {
+  for (auto& kv : g_plans) {
+    Plan& p = kv.second;
     if (p.dev) {
       (void)hipSetDevice(p.device);
       (void)hipDeviceSynchronize();

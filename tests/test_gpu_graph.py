@@ -54,6 +54,13 @@ def test_captured_forward_merge_backward_replays_match_eager():
     bufs = (out_g, lse_g, dq_g, dk_g, dv_g)
     refs = (out, lse, dq, dk, dv)
     other = torch.empty_like(out)
+    # More descriptors than the work-table cache once held (64), each with its own tables: no call may
+    # free a table the graph captured (the cache keeps every table until zl_shutdown).
+    for n in range(1, 81):
+        dn = api.SegDesc([0, n], [0], [0], [1], [0, n], [0], 0)
+        xn = torch.randn((n, 1, 64), dtype=torch.bfloat16, device=dev)
+        api.attn_fwd(dn, xn, xn, xn, 0.125)
+    torch.cuda.synchronize()
     for rep in range(3):
         for b in bufs:
             b.fill_(float("nan"))

@@ -264,3 +264,45 @@ def test_random_descriptors_larger_bf16(seed):
     if not d["kind"] or d["cu_seqlens_q"][-1] == 0:
         pytest.skip("empty draw")
     run_and_compare(d, 3, (64, 128)[seed % 2], torch.bfloat16, 600 + seed)
+
+
+def test_backward_zero_row_shard_writes_zero_dkdv():
+    """The blocks of a SHARD segment without query rows get dK = dV = 0 (no query attends to them),
+    written by the backward: the buffers start as NaN.  The WHOLE segments around it match the oracle."""
+    d = _descs.desc(cu_q=(0, 150, 150, 190), kind=(0, 1, 0), kv_first=(0, 1, 3), kv_count=(1, 2, 1),
+                    cu_k=(0, 150, 350, 420, 460), block_index=(0, 0, 1, 0), num_slots=2)
+    H, hd = 2, 128
+    desc = api.SegDesc.of(d)
+    q, k, v, do = _inputs(d, H, hd, torch.bfloat16, 61)
+    qd, kd_, vd, dod = (t.cuda() for t in (q, k, v, do))
+    scale = hd ** -0.5
+    out, lse, _, _ = api.attn_fwd(desc, qd, kd_, vd, scale)
+    nan = float("nan")
+    dq = torch.full_like(qd, nan)
+    dk, dv = torch.full_like(kd_, nan), torch.full_like(vd, nan)
+    api.attn_bwd(desc, qd, kd_, vd, out, lse, dod, scale, dq, dk, dv)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(dk[150:420]) == 0 and torch.count_nonzero(dv[150:420]) == 0
+    rq, rk, rv = oracle.packed_backward(d, q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                        do.double().numpy(), scale)
+    assert not np.isnan(to64(dq)).any()
+    _check_bwd(dq, rq, "dq")
+    _check_bwd(dk, rk, "dk")
+    _check_bwd(dv, rv, "dv")
+
+
+def test_backward_without_query_rows():
+    """Tq = 0: the only segment is a SHARD with no queries over two blocks; the call launches no
+    preprocess (nothing to reduce) and still zeroes both blocks' dK/dV."""
+    d = _descs.desc(cu_q=(0, 0), kind=(1,), kv_first=(0,), kv_count=(2,), cu_k=(0, 64, 100),
+                    block_index=(0, 1), num_slots=2)
+    H, hd = 3, 64
+    desc = api.SegDesc.of(d)
+    g = torch.Generator().manual_seed(62)
+    k, v = (torch.randn((100, H, hd), generator=g).to(torch.bfloat16).cuda() for _ in range(2))
+    empty = torch.empty((0, H, hd), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((0, H), dtype=torch.float32, device="cuda")
+    dk, dv = torch.full_like(k, float("nan")), torch.full_like(v, float("nan"))
+    api.attn_bwd(desc, empty, k, v, empty, lse, empty, hd ** -0.5, empty, dk, dv)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(dk) == 0 and torch.count_nonzero(dv) == 0

@@ -17,10 +17,11 @@ pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not HAVE_GPU, reason="needs a 
 O_TOL, LSE_TOL = 2e-2, 1e-3
 
 
-def _ring(shard_q, shard_blocks, fillers, fill_step, H, hd, dtype, seed):
+def _ring(shard_q, shard_blocks, fillers, fill_step, H, hd, dtype, seed, block_index_fill=0):
     """shard_q: query count per shard; shard_blocks[s]: key counts of its blocks
     (all shards have the same number of blocks R); fillers: WHOLE lengths;
-    fill_step[f]: the step that carries filler f."""
+    fill_step[f]: the step that carries filler f; block_index_fill: the value
+    of every block_index entry (a ring step does not read them)."""
     R = len(shard_blocks[0])
     g = torch.Generator().manual_seed(seed)
     rnd = lambda n: torch.randn((n, H, hd), generator=g).to(dtype)
@@ -48,7 +49,7 @@ def _ring(shard_q, shard_blocks, fillers, fill_step, H, hd, dtype, seed):
         cu_k = np.concatenate([[0], np.cumsum(lk)]).astype(np.int32)
         nseg = len(lq)
         desc = api.SegDesc(cu_q, np.array(kinds, np.uint8), np.arange(nseg, dtype=np.int32),
-                           np.ones(nseg, np.int32), cu_k, np.zeros(nseg, np.int32), 1)
+                           np.ones(nseg, np.int32), cu_k, np.full(nseg, block_index_fill, np.int32), 1)
         q = torch.cat(qs + [fq[f] for f in fs]).to(dev)
         k = torch.cat([ks[s][r] for s in range(len(shard_q))] + [fk[f] for f in fs]).to(dev)
         v = torch.cat([vs[s][r] for s in range(len(shard_q))] + [fv[f] for f in fs]).to(dev)
@@ -90,6 +91,14 @@ def test_ring_steps_bf16(hd):
     # two shards over four blocks each (one block empty, ragged sizes), fillers in steps 0, 1, 3
     _ring(shard_q=(150, 33), shard_blocks=((300, 0, 129, 64), (64, 191, 1, 256)), fillers=(200, 77, 1),
           fill_step=(0, 1, 3), H=2, hd=hd, dtype=torch.bfloat16, seed=31)
+
+
+def test_ring_steps_ignore_block_index():
+    """A ring step reads no block_index: with every entry -1 (a sentinel a caller might leave there) the
+    shard rows still fold into the accumulator and match the oracle.  (The step plan once took the shard
+    items' slot from block_index, and a negative slot sent them down the WHOLE epilogue.)"""
+    _ring(shard_q=(150, 33), shard_blocks=((300, 0, 129), (64, 191, 1)), fillers=(200,), fill_step=(1,), H=2,
+          hd=128, dtype=torch.bfloat16, seed=36, block_index_fill=-1)
 
 
 def test_ring_steps_first_block_empty_bf16():

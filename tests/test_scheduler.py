@@ -67,3 +67,20 @@ def test_list_schedule_bound(name):
     total = cost.sum()
     assert makespan <= total / m + (1 - 1 / m) * cost.max() + 1e-6
     assert makespan / (total / m) < 1.05
+
+
+def test_zero_row_shard_keeps_its_key_tiles():
+    """A SHARD segment without query rows has no forward or dQ work, but its blocks' dK/dV are outputs
+    of the backward (zero), so the dK/dV schedule still covers them: key tiles of 128 with q_len 0,
+    ordered after every item of positive cost."""
+    d = _descs.desc(cu_q=(0, 100, 100), kind=(0, 1), kv_first=(0, 1), kv_count=(1, 2),
+                    cu_k=(0, 100, 300, 430), block_index=(0, 1, 0), num_slots=2)
+    items, (tm, tn) = api.plan_dump(api.SegDesc.of(d), 1, 128, torch.bfloat16, api.ZL_OP_BWD)
+    assert tn == 128
+    want = [(0, 100, 0, 100, 0, -1, 0, 0),
+            (100, 0, 100, 128, 0, 1, 1, 1), (100, 0, 228, 72, 0, 1, 1, 1),
+            (100, 0, 300, 128, 0, 0, 1, 2), (100, 0, 428, 2, 0, 0, 1, 2)]
+    assert [tuple(int(x) for x in it) for it in items] == want
+    for op in (api.ZL_OP_FWD, api.ZL_OP_BWD_DQ):
+        items, _ = api.plan_dump(api.SegDesc.of(d), 1, 128, torch.bfloat16, op)
+        assert set(items[:, 6].tolist()) == {0}
