@@ -297,6 +297,31 @@ zl_status zl_attn_bwd_step(const zl_seg_desc* desc, int32_t num_heads, int32_t h
                            void* dq, void* dk, void* dv, float* dq_acc, uint32_t flags,
                            void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of the static device scratch zl_attn_bwd_noalloc uses on each GPU. */
+#define ZL_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/*
+ * zl_attn_bwd for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments and results as zl_attn_bwd with flags 0 (bit for bit: the same
+ * work items on the same kernels), but no workspace argument and no
+ * allocation on any call.  The batch's work tables (32 bytes per work item)
+ * and its D / LSE*log2(e) workspace (8 bytes per query row and head, plus
+ * 256-byte alignment) go into one library-owned static device array of
+ * ZL_NOALLOC_SCRATCH_BYTES per GPU, held by every GPU the library runs on
+ * until the process ends.  The tables are built on the host (and cached there
+ * per descriptor) and copied into the array on `stream` by every call.
+ * Errors: as zl_attn_bwd, plus ZL_ERR_WORKSPACE (nothing enqueued) when the
+ * batch needs more than ZL_NOALLOC_SCRATCH_BYTES.  Every call on a GPU uses
+ * that GPU's one array and overwrites what the last call left there: calls
+ * ordered on one stream are safe, calls that overlap on one GPU (other
+ * streams, other host threads) race.  Keep profiling off (it creates events).
+ */
+zl_status zl_attn_bwd_noalloc(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim, zl_dtype dtype,
+                              float softmax_scale, const void* q, const void* k, const void* v,
+                              const void* out, const float* lse, const void* dout,
+                              void* dq, void* dk, void* dv, void* stream);
+
 /*
  * Host-only view of the schedule a launch would use (no device work): the
  * work items of op in issue order, 8 int32 each:

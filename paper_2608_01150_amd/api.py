@@ -93,6 +93,8 @@ _merge_ex = _sig("zl_lse_merge_ex", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_
                  _vp, ctypes.c_int32, _vp, _vp, _vp)
 _bwd = _sig("zl_attn_bwd", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
             _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_uint32, _vp, ctypes.c_size_t, _vp)
+_bwd_noalloc = _sig("zl_attn_bwd_noalloc", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int,
+                    ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp)
 _bwd_step = _sig("zl_attn_bwd_step", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_float,
                  _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_uint32, _vp, ctypes.c_size_t, _vp)
 _plan_dump = _sig("zl_plan_dump", ctypes.c_int, _DP, ctypes.c_int32, ctypes.c_int32, ctypes.c_int, ctypes.c_int32,
@@ -457,6 +459,22 @@ def attn_bwd(desc: SegDesc, q, k, v, out, lse, dout, scale: float, dq=None, dk=N
         workspace = torch.empty(workspace_size(desc, h, d, q.dtype, ZL_OP_BWD), dtype=torch.uint8, device=dev)
     _check(_bwd(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
                 _p(dout), _p(dq), _p(dk), _p(dv), 0, _p(workspace), workspace.numel() * workspace.element_size(), _stream(dev)))
+    return dq, dk, dv
+
+
+def attn_bwd_noalloc(desc: SegDesc, q, k, v, out, lse, dout, scale: float, dq, dk, dv):
+    """zl_attn_bwd_noalloc: zl_attn_bwd with no allocation anywhere (the library's static scratch
+    holds its tables and workspace).  Every output is caller-provided; returns (dq, dk, dv)."""
+    h, d = _qkv(desc, q, k, v)
+    tq, tk = desc.total_q, desc.total_k
+    for t, name in ((out, "out"), (dout, "dout"), (dq, "dq")):
+        _need(t, name, (tq, h, d), q.dtype)
+    for t, name in ((dk, "dk"), (dv, "dv")):
+        _need(t, name, (tk, h, d), q.dtype)
+    _need(lse, "lse", (tq, h), torch.float32)
+    dev = _same_gpu(q, k, v, out, lse, dout, dq, dk, dv)
+    _check(_bwd_noalloc(desc.ptr(), h, d, _dtype_code(q.dtype), float(scale), _p(q), _p(k), _p(v), _p(out), _p(lse),
+                        _p(dout), _p(dq), _p(dk), _p(dv), _stream(dev)))
     return dq, dk, dv
 
 

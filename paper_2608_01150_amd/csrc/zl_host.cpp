@@ -372,6 +372,23 @@ zl_status get_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int
   return insert_plan(std::move(key), std::move(p), stream, out);
 }
 
+// Host-only plans (no device copy) for callers that bring their own device
+// memory for the tables: built once per descriptor and kept until
+// zl_shutdown, like the device tables.  Caller holds g_mu.
+std::unordered_map<std::vector<int64_t>, Plan, KeyHash> g_host_plans;
+
+zl_status get_host_plan(const zl_seg_desc* d, int32_t H, int32_t hd, zl_dtype dt, int op, const Plan** out) {
+  std::vector<int64_t> key = plan_key(d, H, hd, dt, op, -1);
+  auto hit = g_host_plans.find(key);
+  if (hit == g_host_plans.end()) {
+    Plan p;
+    zl_status st = build_plan_host(d, H, dt, op, p);
+    if (st != ZL_OK) return st;
+    hit = g_host_plans.emplace(std::move(key), std::move(p)).first;
+  }
+  *out = &hit->second;
+  return ZL_OK;
+}
 
 // Uploads a built plan (stream-ordered, from its own host copy, which the
 // cache keeps alive) and caches it.  Caller holds g_mu.
@@ -871,6 +888,35 @@ zl_status attn_bwd_impl(const BwdCall& c, void* workspace, size_t ws_bytes, void
 
 }  // namespace
 
+namespace zl {
+
+zl_status attn_bwd_scratch(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
+                           const void* k, const void* v, const void* out, const float* lse, const void* dout, void* dq,
+                           void* dk, void* dv, size_t scratch_bytes, ScratchFn acquire, void* stream) {
+  const BwdCall c{desc, H, hd, dt, scale, q, k, v, out, lse, dout, dq, dk, dv, false, nullptr, 0u};
+  Shape sh;
+  zl_status st = validate_bwd(c, &sh);
+  if (st != ZL_OK) return st;
+  std::lock_guard<std::mutex> lock(g_mu);
+  const Plan* hp = nullptr;
+  if ((st = get_host_plan(desc, H, hd, dt, ZL_OP_BWD, &hp)) != ZL_OK) return st;
+  // layout: [dK/dV items | dQ items] (the plan's host bytes), then the workspace
+  const size_t tables = align256(hp->host.size());
+  const size_t need = tables + bwd_workspace_bytes(sh, H);
+  if (need > scratch_bytes)
+    return fail(ZL_ERR_WORKSPACE, "this batch needs %zu bytes of scratch (work tables %zu, workspace %zu); the "
+                "static scratch holds %zu", need, tables, need - tables, scratch_bytes);
+  void* base = nullptr;
+  if ((st = acquire(&base)) != ZL_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!hp->host.empty() &&
+      hipMemcpyAsync(base, hp->host.data(), hp->host.size(), hipMemcpyHostToDevice, s) != hipSuccess)
+    return fail(ZL_ERR_HIP, "copy of the work tables into the scratch failed");
+  return launch_bwd(c, sh, base, hp->slots_offset, hp->n_items, hp->n_items2, static_cast<char*>(base) + tables, s);
+}
+
+}  // namespace zl
+
 extern "C" {
 
 zl_status zl_attn_bwd(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
@@ -967,6 +1013,7 @@ void zl_shutdown(void) {
     }
   }
   g_plans.clear();
+  g_host_plans.clear();
   if (have_dev) (void)hipSetDevice(cur);
 }
 

@@ -143,6 +143,17 @@ struct UlyssesParams {
 };
 
 hipError_t launch_merge(const MergeParams& p, int head_dim, bool out_bf16, bool part_bf16, hipStream_t s);
+
+// Returns the calling thread's current device's scratch address in *ptr.
+typedef zl_status (*ScratchFn)(void** ptr);
+
+// zl_attn_bwd with its work tables and its D / LSE*log2(e) workspace in one
+// block of device scratch of scratch_bytes, obtained from `acquire` once the
+// call is validated and known to fit; the tables are built on the host
+// (cached per descriptor) and copied in on the stream.  No allocation.
+zl_status attn_bwd_scratch(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtype dt, float scale, const void* q,
+                           const void* k, const void* v, const void* out, const float* lse, const void* dout, void* dq,
+                           void* dk, void* dv, size_t scratch_bytes, ScratchFn acquire, void* stream);
 hipError_t launch_ulysses(const UlyssesParams& p, int op, int head_dim, hipStream_t s);
 // stage 0: preprocess (D), 1: dK/dV, 2: dQ
 hipError_t launch_bwd_bf16(const BwdParams& p, int head_dim, int stage, hipStream_t s);
