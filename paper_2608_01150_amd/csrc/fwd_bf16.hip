@@ -30,10 +30,107 @@ namespace {
 constexpr int BN = kFwdTileN;
 constexpr int NT = 512;
 
-// Rescale the running output only when the running maximum grows by more
-// than 2^8 (log2 units): exp2 of scores against a stale maximum stays below
-// 2^8, exact in fp32 and bf16 range, and O and l share the same reference.
-constexpr float kRescaleSlack = 8.f;
+// Scores are exponentiated against the running maximum as it stands, without
+// first taking the new block's maximum.  While the block's scores exceed it by
+// at most 64 (log2 units) every P stays within 2^64 and O, l sum it exactly as
+// against any other common reference (fp32 keeps its relative precision far
+// beyond that).  A block whose exponentials sum (per lane: 16 of a query's
+// keys) past 2^64 (+inf included, as for the first block against the initial
+// -1e30) takes a slow path: its true maximum, a rescale of O and l to it, and
+// its exponentials again.  So the common path needs one compare per block in
+// place of a max over its scores.
+constexpr float kSumBound = 0x1p64f;
+
+// Epilogue of a forward item: normalises the running output of this lane's
+// query and stores it by the item's kind.  o[db][i] is (d = db*32 +
+// 16*(i/8) + 8*g + i%8, query qr); m_run is the running maximum (log2
+// units) and l_part this lane's half of the row sum.
+template <int D>
+__device__ __forceinline__ void fwd_store(const FwdParams& p, const Item& it, int qr, bool q_ok, int g,
+                                          const f32x16 (&o)[D / 32], float m_run, float l_part) {
+  const float l = xor32_sum(l_part);
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  const float lse = l > 0.f ? (m_run + __log2f(l)) * kLn2 : -INFINITY;
+  if (!q_ok) return;
+  const int64_t row = (int64_t)(it.q_start + qr) * p.num_heads + it.head;
+  if (it.slot < 0) {
+    uint16_t* og = static_cast<uint16_t*>(p.out) + row * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        u32x4 w;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[t] = pack_bf16(o[db][8 * h + 2 * t] * inv, o[db][8 * h + 2 * t + 1] * inv);
+        *reinterpret_cast<u32x4*>(og + db * 32 + 16 * h + 8 * g) = w;
+      }
+    }
+    if (g == 0) p.lse[row] = lse;
+  } else if (p.step_mode) {
+    // Ring step: fold this block (O_b = o * inv, LSE_b = lse) into the
+    // running accumulator; the last step writes the final output instead.
+    float* acc = p.o_acc + row * D;
+    float wa, wb, lse_new;
+    step_weights(p.step_first, p.step_first ? 0.f : p.lse_acc[row], lse, wa, wb, lse_new);
+    wb *= inv;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int c0 = db * 32 + 16 * h + 8 * g;
+        f32x4 a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
+        if (!p.step_first) {
+          a = *reinterpret_cast<const f32x4*>(acc + c0);
+          b = *reinterpret_cast<const f32x4*>(acc + c0 + 4);
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          a[t] = wa * a[t] + wb * o[db][8 * h + t];
+          b[t] = wa * b[t] + wb * o[db][8 * h + 4 + t];
+        }
+        if (p.step_last) {
+          u32x4 w = {pack_bf16(a[0], a[1]), pack_bf16(a[2], a[3]), pack_bf16(b[0], b[1]), pack_bf16(b[2], b[3])};
+          *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.out) + row * D + c0) = w;
+        } else {
+          *reinterpret_cast<f32x4*>(acc + c0) = a;
+          *reinterpret_cast<f32x4*>(acc + c0 + 4) = b;
+        }
+      }
+    }
+    if (g == 0) (p.step_last ? p.lse : p.lse_acc)[row] = lse_new;
+  } else if (p.part_bf16) {
+    // bf16 partial: this lane's 8 consecutive d values in one 16-byte store
+    uint16_t* og = static_cast<uint16_t*>(p.o_part) + it.slot * p.slot_stride + row * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        u32x4 w;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[t] = pack_bf16(o[db][8 * h + 2 * t] * inv, o[db][8 * h + 2 * t + 1] * inv);
+        *reinterpret_cast<u32x4*>(og + db * 32 + 16 * h + 8 * g) = w;
+      }
+    }
+    if (g == 0) p.lse_part[it.slot * p.lse_slot_stride + row] = lse;
+  } else {
+    float* og = static_cast<float*>(p.o_part) + it.slot * p.slot_stride + row * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        f32x4 a, b;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          a[t] = o[db][8 * h + t] * inv;
+          b[t] = o[db][8 * h + 4 + t] * inv;
+        }
+        *reinterpret_cast<f32x4*>(og + db * 32 + 16 * h + 8 * g) = a;
+        *reinterpret_cast<f32x4*>(og + db * 32 + 16 * h + 8 * g + 4) = b;
+      }
+    }
+    if (g == 0) p.lse_part[it.slot * p.lse_slot_stride + row] = lse;
+  }
+}
 
 template <int D>
 __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
@@ -124,40 +221,14 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     // s[kb][i] is the raw score of (key kb*32 + 16*(i/8) + 8*g + i%8, query qr).
     f32x16 s[2];
     u32x4 pb[2][2];
-    float lsum = 0.f;
-    // Max of block kb (keys past the range masked on a partial tile) and the
-    // lazy rescale; a rescale after block 0 was exponentiated also rescales
-    // block 0's packed P, which has not yet entered the PV MFMAs.
-    auto block_max = [&](int kb) {
+    float lsum[2] = {0.f, 0.f};
+    // Keys past the range on a partial tile: score -inf, exact at any positive scale.
+    auto mask = [&](int kb) {
       if (nvalid < BN) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int key = kb * 32 + 16 * (i >> 3) + 8 * g + (i & 7);
-          if (key >= nvalid) s[kb][i] = -INFINITY;  // exact at any positive scale
-        }
-      }
-      float mt = s[kb][0];
-#pragma unroll
-      for (int i = 1; i < 16; ++i) mt = fmaxf(mt, s[kb][i]);
-      mt = xor32_max(mt) * p.scale_log2;
-      if (__any(mt > m_run + kRescaleSlack)) {
-        const float m_new = fmaxf(m_run, mt);
-        const float alpha = fast_exp2(m_run - m_new);
-        m_run = m_new;
-        l_part *= alpha;
-        lsum *= alpha;
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-          for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
-        }
-        if (kb == 1) {
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-              pb[0][h][t] = pack_bf16(bf16_lo(pb[0][h][t]) * alpha, bf16_hi(pb[0][h][t]) * alpha);
-          }
+          if (key >= nvalid) s[kb][i] = -INFINITY;
         }
       }
     };
@@ -165,8 +236,32 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     auto expo = [&](int kb, int c) {
       const float e0 = fast_exp2(fmaf(s[kb][2 * c], p.scale_log2, -m_run));
       const float e1 = fast_exp2(fmaf(s[kb][2 * c + 1], p.scale_log2, -m_run));
-      lsum += e0 + e1;
+      lsum[kb] += e0 + e1;
       pb[kb][c >> 2][c & 3] = pack_bf16(e0, e1);
+    };
+    // The slow path of block kb (see kSumBound): when it is taken for block 1,
+    // block 0 has entered O already, and the rescale covers it there.
+    auto block_fix = [&](int kb) {
+      float mt = s[kb][0];
+#pragma unroll
+      for (int i = 1; i < 16; ++i) mt = fmaxf(mt, s[kb][i]);
+      mt = xor32_max(mt) * p.scale_log2;
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = fast_exp2(m_run - m_new);
+      m_run = m_new;
+      l_part *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+      }
+      lsum[kb] = 0.f;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) expo(kb, c);
+    };
+    auto block_done = [&](int kb) {
+      if (__any(lsum[kb] > kSumBound)) block_fix(kb);
+      l_part += lsum[kb];
     };
 
     u32x4 ring[PF];
@@ -174,9 +269,9 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     for (int j = 0; j < PF; ++j) ring[j] = a_op(j);
     s[0] = s[1] = f32x16{};
     __builtin_amdgcn_sched_barrier(0);
-    // Raised issue priority while this wave's MFMA loops run, lowered for the
-    // VALU-only max of block 1: when the SIMD's two waves drift apart, the one
-    // with MFMAs ready issues first and keeps the matrix core fed.
+    // Raised issue priority while this wave's MFMA loops run: when the SIMD's
+    // two waves drift apart, the one with MFMAs ready issues first and keeps
+    // the matrix core fed.
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int j = 0; j < NS; ++j) {
@@ -185,19 +280,19 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       const int kb = j / (NS / 2);
       s[kb] = mfma32(a, qf[j % (NS / 2)], s[kb]);
       if (j % DMA_GAP == 1 && j / DMA_GAP < DMA_PER_FETCH) dma.issue_one(next_rsrc, next_lds, j / DMA_GAP);
-      // Block 1's MFMAs carry block 0's softmax: the max first, then the
-      // eight exponential pairs spread over the remaining slots.  Each packed
-      // word and the running sum are pinned where they are computed: block
-      // 1's partial-tile mask is a branch, and without the pin the compiler
+      // Block 1's MFMAs carry block 0's softmax: the mask of a partial tile
+      // first, then the eight exponential pairs spread over the remaining
+      // slots.  Each packed word and the block's sum are pinned where they are
+      // computed: block 1's mask is a branch, and without the pin the compiler
       // sinks this work past it, next to its first use, out of the MFMAs.
-      if (j == NS / 2) block_max(0);
+      if (j == NS / 2) mask(0);
       if (j > NS / 2) {
         constexpr int SLOTS = NS / 2 - 1;
         const int c0 = (j - NS / 2 - 1) * 8 / SLOTS, c1 = (j - NS / 2) * 8 / SLOTS;
 #pragma unroll
         for (int c = c0; c < c1; ++c) {
           expo(0, c);
-          asm volatile("" : "+v"(pb[0][c >> 2][c & 3]), "+v"(lsum));
+          asm volatile("" : "+v"(pb[0][c >> 2][c & 3]), "+v"(lsum[0]));
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -205,25 +300,25 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     u32x4 cring[PFC];
 #pragma unroll
     for (int m = 0; m < PFC; ++m) cring[m] = c_op(m);
-    __builtin_amdgcn_s_setprio(0);
-    block_max(1);
-    __builtin_amdgcn_s_setprio(1);
+    block_done(0);
+    mask(1);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int m = 0; m < NP; ++m) {
       const u32x4 a = cring[m % PFC];
       if (m + PFC < NP) cring[m % PFC] = c_op(m + PFC);
-      // Block 0's PV MFMAs carry block 1's exponentials.
+      // Block 0's PV MFMAs carry block 1's exponentials; block 1's sum is
+      // checked before its own PV MFMAs.
       if (m < NP / 2) {
 #pragma unroll
         for (int c = m * 8 / (NP / 2); c < (m + 1) * 8 / (NP / 2); ++c) expo(1, c);
       }
+      if (m == NP / 2) block_done(1);
       const int kb = m / (NP / 2), db = (m % (NP / 2)) >> 1, s2 = m & 1;
       o[db] = mfma32(a, pb[kb][s2], o[db]);
       __builtin_amdgcn_sched_barrier(0);
     }
     __builtin_amdgcn_s_setprio(0);
-    l_part += lsum;
   };
 
   // A wave with no query rows in this item (the ragged last tile of a
@@ -272,89 +367,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     wait_vmem();  // the lookahead loads must land before the workgroup's LDS is released
   }
 
-  // Epilogue.  o[db][i] is (d = db*32 + 16*(i/8) + 8*g + i%8, query qr).
-  const float l = xor32_sum(l_part);
-  const float inv = l > 0.f ? 1.f / l : 0.f;
-  const float lse = l > 0.f ? (m_run + __log2f(l)) * kLn2 : -INFINITY;
-  if (!q_ok) return;
-  const int64_t row = (int64_t)(it.q_start + qr) * p.num_heads + it.head;
-  if (it.slot < 0) {
-    uint16_t* og = static_cast<uint16_t*>(p.out) + row * D;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        u32x4 w;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) w[t] = pack_bf16(o[db][8 * h + 2 * t] * inv, o[db][8 * h + 2 * t + 1] * inv);
-        *reinterpret_cast<u32x4*>(og + db * 32 + 16 * h + 8 * g) = w;
-      }
-    }
-    if (g == 0) p.lse[row] = lse;
-  } else if (p.step_mode) {
-    // Ring step: fold this block (O_b = o * inv, LSE_b = lse) into the
-    // running accumulator; the last step writes the final output instead.
-    float* acc = p.o_acc + row * D;
-    float wa, wb, lse_new;
-    step_weights(p.step_first, p.step_first ? 0.f : p.lse_acc[row], lse, wa, wb, lse_new);
-    wb *= inv;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int c0 = db * 32 + 16 * h + 8 * g;
-        f32x4 a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
-        if (!p.step_first) {
-          a = *reinterpret_cast<const f32x4*>(acc + c0);
-          b = *reinterpret_cast<const f32x4*>(acc + c0 + 4);
-        }
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          a[t] = wa * a[t] + wb * o[db][8 * h + t];
-          b[t] = wa * b[t] + wb * o[db][8 * h + 4 + t];
-        }
-        if (p.step_last) {
-          u32x4 w = {pack_bf16(a[0], a[1]), pack_bf16(a[2], a[3]), pack_bf16(b[0], b[1]), pack_bf16(b[2], b[3])};
-          *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.out) + row * D + c0) = w;
-        } else {
-          *reinterpret_cast<f32x4*>(acc + c0) = a;
-          *reinterpret_cast<f32x4*>(acc + c0 + 4) = b;
-        }
-      }
-    }
-    if (g == 0) (p.step_last ? p.lse : p.lse_acc)[row] = lse_new;
-  } else if (p.part_bf16) {
-    // bf16 partial: this lane's 8 consecutive d values in one 16-byte store
-    uint16_t* og = static_cast<uint16_t*>(p.o_part) + it.slot * p.slot_stride + row * D;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        u32x4 w;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) w[t] = pack_bf16(o[db][8 * h + 2 * t] * inv, o[db][8 * h + 2 * t + 1] * inv);
-        *reinterpret_cast<u32x4*>(og + db * 32 + 16 * h + 8 * g) = w;
-      }
-    }
-    if (g == 0) p.lse_part[it.slot * p.lse_slot_stride + row] = lse;
-  } else {
-    float* og = static_cast<float*>(p.o_part) + it.slot * p.slot_stride + row * D;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        f32x4 a, b;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          a[t] = o[db][8 * h + t] * inv;
-          b[t] = o[db][8 * h + 4 + t] * inv;
-        }
-        *reinterpret_cast<f32x4*>(og + db * 32 + 16 * h + 8 * g) = a;
-        *reinterpret_cast<f32x4*>(og + db * 32 + 16 * h + 8 * g + 4) = b;
-      }
-    }
-    if (g == 0) p.lse_part[it.slot * p.lse_slot_stride + row] = lse;
-  }
+  fwd_store<D>(p, it, qr, q_ok, g, o, m_run, l_part);
 }
 
 }  // namespace
