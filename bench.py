@@ -302,6 +302,26 @@ def merge_record(w, H, hd, partials, ms):
             "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": mbytes, "ms": round(ms, 4)}
 
 
+def copy_ceiling(mib=1024, reps=10):
+    """Device-to-device copy rate (torch copy_, read + write bytes) on this GPU in this run: a measured
+    ceiling for HBM-bound kernels such as the merge."""
+    import torch
+    src = torch.ones(mib << 20, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    del src, dst
+    return {"kind": f"device copy of {mib} MiB (torch copy_)", "gbs": round(2.0 * (mib << 20) / (ms * 1e-3) / 1e9, 1)}
+
+
 def gemm_ceiling(n=8192, reps=10):
     """bf16 GEMM rate (torch.matmul, hipBLASLt) on this GPU in this run: a measured ceiling for dense
     bf16 MFMA work with no attention dependencies."""
@@ -512,6 +532,10 @@ def main():
         rec["merge_kernel"]["workload"] = w.name
     elif args.mode == "blocks" and args.merge_reps > 0:
         rec["merge_kernel"] = merge_on(args.merge_workload, args.merge_reps, args.partials)
+    if "merge_kernel" in rec and not args.no_ceiling:
+        cc = copy_ceiling()
+        rec["merge_kernel"]["measured_ceiling"] = cc
+        rec["merge_kernel"]["frac_of_measured_ceiling"] = round(rec["merge_kernel"]["achieved"] / cc["gbs"], 4)
     # Host scheduler: building the forward, dK/dV and dQ work tables of this batch (what the cached
     # plan saves on every later call; zl_plan_dump runs the same builder on the host).
     t0 = time.perf_counter()

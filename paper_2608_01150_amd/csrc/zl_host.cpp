@@ -509,15 +509,24 @@ hipError_t timed(int kid, hipStream_t s, F&& launch) {
   return e;
 }
 
-// Work items per XCD run of the dispatch order (see dispatch_item): read
-// once from ZL_XCD_CHUNK, default 1 (plain hardware order).
-int32_t xcd_chunk() {
-  static const int32_t v = [] {
+// Work items per XCD run of the dispatch order (see dispatch_item).  The
+// hardware hands consecutive workgroups to the 8 XCDs in turn, and each XCD
+// has its own L2.  In a launch of WHOLE segments only, a segment's tiles of one
+// head are consecutive in the work table (equal cost, ties by query or key
+// tile) and read the same K/V (or Q/dO) tiles, so runs of 16 keep them on one
+// XCD, where they share that data through its L2.  With SHARD segments the
+// tie-break orders a shard's items by query tile, then block, so plain order
+// (1) already sends block j of every query tile to XCD j mod 8 and the block's
+// K/V stays in one L2; longer runs would mix blocks there.  ZL_XCD_CHUNK (read
+// once, 1..4096) overrides the choice for every launch.
+int32_t xcd_chunk(const Shape& sh) {
+  static const int32_t env = [] {
     const char* e = std::getenv("ZL_XCD_CHUNK");
-    const long x = e ? std::strtol(e, nullptr, 10) : 1;
-    return (int32_t)(x >= 1 && x <= 4096 ? x : 1);
+    const long x = e ? std::strtol(e, nullptr, 10) : 0;
+    return (int32_t)(x >= 1 && x <= 4096 ? x : 0);
   }();
-  return v;
+  if (env) return env;
+  return sh.any_shard_rows ? 1 : 16;
 }
 
 zl_status hip_status(hipError_t e, const char* what) {
@@ -596,7 +605,7 @@ zl_status zl_attn_fwd_ex(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtyp
   p.lse_slot_stride = (int64_t)sh.total_q * H;
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
-  p.xcd_chunk = xcd_chunk();
+  p.xcd_chunk = xcd_chunk(sh);
   hipError_t e = timed(ZL_K_FWD, s, [&] {
     return dt == ZL_BF16 ? zl::launch_fwd_bf16(p, hd, s) : zl::launch_fwd_fp32(p, hd, s);
   });
@@ -639,7 +648,7 @@ zl_status zl_attn_fwd_step(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dt
   p.num_heads = H;
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
-  p.xcd_chunk = xcd_chunk();
+  p.xcd_chunk = xcd_chunk(sh);
   p.step_mode = 1;
   p.step_first = first;
   p.step_last = last;
@@ -858,7 +867,7 @@ zl_status launch_bwd(const BwdCall& c, const Shape& sh, const void* tables, size
   p.total_q = sh.total_q;
   p.scale = c.scale;
   p.scale_log2 = c.scale * 1.4426950408889634f;
-  p.xcd_chunk = xcd_chunk();
+  p.xcd_chunk = xcd_chunk(sh);
   p.step_mode = c.step && !(first && last) ? 1 : 0;
   p.step_first = first ? 1 : 0;
   p.step_last = last ? 1 : 0;

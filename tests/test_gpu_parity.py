@@ -306,3 +306,32 @@ def test_backward_without_query_rows():
     api.attn_bwd(desc, empty, k, v, empty, lse, empty, hd ** -0.5, empty, dk, dv)
     torch.cuda.synchronize()
     assert torch.count_nonzero(dk) == 0 and torch.count_nonzero(dv) == 0
+
+
+def test_forward_running_max_jumps():
+    """The forward exponentiates a block against the running maximum as it stands and rescales only when
+    the block's sum of exponentials passes 2^64.  All queries share one direction u; keys that are
+    multiples f*u score about 17.8*f (log2 units) against ~5 for the others.  In a 600-key segment the
+    maximum then rises by ~13 (key 40, block 1 of tile 0: common path, P up to 2^13), ~89 (key 200,
+    block 0 of tile 3: slow path), ~54 (key 300, block 1 of tile 4: common path with P near 2^54), ~89
+    (key 500, block 1 of tile 7: slow path after block 0 has entered O) and ~107 (key 530, block 0 of
+    tile 8: slow path).  An 80-key segment jumps by ~48 in its second tile (common path).  Both must
+    match the oracle."""
+    H, hd = 2, 128
+    g = torch.Generator().manual_seed(63)
+    u = torch.randn((1, H, hd), generator=g)
+    d = _descs.desc(cu_q=(0, 600, 680), kind=(0, 0), kv_first=(0, 1), kv_count=(1, 1), cu_k=(0, 600, 680),
+                    block_index=(0, 0), num_slots=0)
+    q = (u + 0.05 * torch.randn((680, H, hd), generator=g)).to(torch.bfloat16)
+    k = torch.randn((680, H, hd), generator=g)
+    v = torch.randn((680, H, hd), generator=g).to(torch.bfloat16)
+    for key, f in ((40, 1.0), (200, 6.0), (300, 9.0), (500, 14.0), (530, 20.0), (600 + 70, 3.0)):
+        k[key] = f * u[0]
+    k = k.to(torch.bfloat16)
+    desc = api.SegDesc.of(d)
+    scale = hd ** -0.5
+    out, lse, _, _ = api.attn_fwd(desc, q.cuda(), k.cuda(), v.cuda(), scale)
+    torch.cuda.synchronize()
+    ref = oracle.packed_forward(d, q.double().numpy(), k.double().numpy(), v.double().numpy(), scale)
+    np.testing.assert_allclose(to64(out), ref["out"], rtol=0, atol=O_TOL)
+    np.testing.assert_allclose(to64(lse), ref["lse"], rtol=0, atol=LSE_TOL)
