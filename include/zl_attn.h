@@ -120,7 +120,7 @@ int32_t zl_abi_version(void);
 const char* zl_last_error(void);
 
 /* Device workspace in bytes that zl_attn_bwd needs for this batch (op =
- * ZL_OP_BWD: fp32 D = rowsum(dO*O) and LSE*log2(e), each [Tq,H]); 0 for
+ * ZL_OP_BWD: fp32 -D = -rowsum(dO*O) and LSE*log2(e), each [Tq,H]); 0 for
  * ZL_OP_FWD.  Validates like the call it sizes. */
 zl_status zl_workspace_size(const zl_seg_desc* desc, int32_t num_heads, int32_t head_dim,
                             zl_dtype dtype, int32_t op, size_t* bytes);

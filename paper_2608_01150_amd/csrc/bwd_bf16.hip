@@ -1,8 +1,9 @@
 // Packed whole+shard attention backward, bf16 inputs, gfx950 MFMA.
 //
 // Three launches on one stream, no atomics (results are deterministic):
-//   1. preprocess  D_i = dO_i . O_i in fp32 for every query row and head, and
-//                  LSE_i in log2 units for the dK/dV kernel's staging.
+//   1. preprocess  -D_i = -dO_i . O_i in fp32 for every query row and head
+//                  (the dP MFMAs start their accumulation from it, so they
+//                  produce dP - D directly), and LSE_i in log2 units.
 //   2. dK/dV       one workgroup per item = up to 128 keys of one head of one
 //                  K/V range, looping over every query of the owning segment
 //                  in steps of 64 rows.  One key per lane:
@@ -52,7 +53,7 @@ __global__ __launch_bounds__(NT) void bwd_pre_kernel(BwdParams p) {
 #pragma unroll
   for (int off = LPU / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
   if (live && sub == 0) {
-    p.dsum[u] = acc;
+    p.dsum[u] = -acc;
     p.lse2[u] = p.lse[u] * 1.4426950408889634f;
   }
 }
@@ -167,7 +168,15 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
       const char* qa = qs[b] + a_off + 32 * ka * PITCH;
       const char* oa = dos[b] + a_off + 32 * ka * PITCH;
       auto a_op = [&](int j) { return *reinterpret_cast<const u32x4*>(((j & 1) ? oa : qa) + poff<D>(0, (j >> 1) * 16)); };
-      f32x4 lsv[2][2], dsv[2][2];
+      // dP of sub-block k accumulates onto -D of its queries (staged with the
+      // tile, in the accumulator's register order: register i <-> query
+      // 16*(i/8) + 8g + i%8 of the sub-block), so it comes out as dP - D.
+      f32x4 nd[2][2], lsv[2][2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) nd[h][e] = *reinterpret_cast<const f32x4*>(&dss[b][ka * 32 + 16 * h + 8 * g + 4 * e]);
+      }
       u32x4 pp[2], pds[2];
       u32x4 ring[PFA];
 #pragma unroll
@@ -176,15 +185,14 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
 #pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            const int q4 = sbb * 32 + 16 * h + 8 * g + 4 * e;
-            lsv[h][e] = *reinterpret_cast<const f32x4*>(&lss[bb][q4]);
-            dsv[h][e] = *reinterpret_cast<const f32x4*>(&dss[bb][q4]);
-          }
+          for (int e = 0; e < 2; ++e)
+            lsv[h][e] = *reinterpret_cast<const f32x4*>(&lss[bb][sbb * 32 + 16 * h + 8 * g + 4 * e]);
         }
       }
       __builtin_amdgcn_sched_barrier(0);
-      f32x16 s = f32x16{}, d_ = f32x16{};
+      f32x16 s = f32x16{}, d_;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) d_[i] = nd[i >> 3][(i >> 2) & 1][i & 3];
 #pragma unroll
       for (int j = 0; j < NM; ++j) {
         const u32x4 a = ring[j % PFA];
@@ -203,9 +211,8 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
           for (int e = 0; e < 2; ++e) {
             const int tt = 2 * t2 + e, i = 8 * h + tt;
             const float l2 = lsv[h][tt >> 2][tt & 3];
-            const float dd = dsv[h][tt >> 2][tt & 3];
             pv[e] = fast_exp2(fmaf(sc[1 - ka][i], p.scale_log2, -l2));
-            dv_[e] = pv[e] * (dp[1 - ka][i] - dd);
+            dv_[e] = pv[e] * dp[1 - ka][i];  // dp already holds dP - D
           }
           pp[h][t2] = pack_bf16(pv[0], pv[1]);
           pds[h][t2] = pack_bf16(dv_[0], dv_[1]);
@@ -378,7 +385,14 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
     of[kk] = q_ok ? *reinterpret_cast<const u32x4*>(dog + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
   }
   const float lse2 = q_ok ? p.lse2[qrow] : 1.0e30f;  // +big: P = 0
-  const float dd = q_ok ? p.dsum[qrow] : 0.f;
+  // -D of this lane's query, as the starting accumulator of every dP^T
+  // block (all 16 registers hold the same query), so the MFMAs give dP - D.
+  f32x16 negd;
+  {
+    const float nd = q_ok ? p.dsum[qrow] : 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) negd[i] = nd;
+  }
   f32x16 dq[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) dq[db] = f32x16{};
@@ -443,14 +457,14 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
       for (int u = 0; u < 2; ++u)
         e[u] = __builtin_amdgcn_fmed3f(fast_exp2(fmaf(sc[kb][i + u], p.scale_log2, -lse2)), 0.f, 1.f) *
-               (dpc[kb][i + u] - dd);
+               dpc[kb][i + u];
       pds[kb][i >> 3][(i & 7) >> 1] = pack_bf16(e[0], e[1]);
     };
     u32x4 ring[PF];
 #pragma unroll
     for (int j = 0; j < PF; ++j) ring[j] = a_op(j);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) sc[kb] = dpc[kb] = f32x16{};
+    for (int kb = 0; kb < 2; ++kb) sc[kb] = f32x16{};
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < NSD; ++j) {
@@ -458,7 +472,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
       if (j + PF < NSD) ring[j % PF] = a_op(j + PF);
       const int kb = j / (NSD / 2), kk = (j % (NSD / 2)) >> 1;
       if (j & 1)
-        dpc[kb] = mfma32(a, of[kk], dpc[kb]);
+        dpc[kb] = mfma32(a, of[kk], kk == 0 ? negd : dpc[kb]);
       else
         sc[kb] = mfma32(a, qf[kk], sc[kb]);
       if (j % DMA_GAP == 1 && j / DMA_GAP < DMA_PER_FETCH) dma.issue_one(next_rsrc, next_lds, j / DMA_GAP);

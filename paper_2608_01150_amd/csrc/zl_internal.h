@@ -104,7 +104,7 @@ struct BwdParams {
   void* dq;
   void* dk;
   void* dv;
-  float* dsum;                 // [Tq, H] fp32 workspace: D = rowsum(dO * O)
+  float* dsum;                 // [Tq, H] fp32 workspace: -D = -rowsum(dO * O)
   float* lse2;                 // [Tq, H] fp32 workspace: LSE * log2(e)
   const Item* kv_items;        // dK/dV items: one key tile against all of its segment's queries
   int32_t n_kv_items;
