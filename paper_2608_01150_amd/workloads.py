@@ -13,11 +13,17 @@ Generator.  Every element of every tensor is a pure function of
 (seed, tensor id, flat element index), so any slice can be drawn on its own,
 on the CPU or on a GPU, with bit-identical values.  The hash is Wellons'
 "lowbias32" 32-bit integer mixer (xorshift-multiply, constants 0x7feb352d
-and 0x846ca68b), evaluated with int64 arithmetic that never overflows.  Two
-hashes give four 16-bit uniforms; their centred sum (Irwin-Hall of order 4)
-scaled to unit variance is an approximately N(0,1) value with exactly
-reproducible arithmetic (an integer below 2^18 times one fp32 constant),
-then rounded once to bf16 (round to nearest even) for bf16 workloads.
+and 0x846ca68b), evaluated with int64 arithmetic that never overflows.  Its
+32 bits pick a point of the standard normal's quantile function: the top 20
+select one of 2^20 equal-probability bins and the low 12 a position inside
+it, where the quantile is interpolated linearly between the bin's edges.  The
+edge table is computed once per process in fp64 (scipy's ndtri; the two outer
+edges are the quantiles at a quarter of a bin from each end), rounded once to
+fp32 and shared by every device, and the interpolation is one fp32 multiply
+and one add, so CPU and GPU draws agree bit for bit.  The samples follow
+N(0,1) to within the curvature of the quantile function inside a bin of
+probability 2^-20, tails included, out to about +-5.06 sigma; they are then
+rounded once to bf16 (round to nearest even) for bf16 workloads.
 """
 from __future__ import annotations
 
@@ -59,17 +65,37 @@ def _lowbias32_int(x: int) -> int:
     return x
 
 
-_IH4_SCALE = 1.0 / 37837.2270  # 1 / sqrt(4 * (65536^2 - 1) / 12)
+_QBITS = 20                       # equal-probability bins of the quantile table
+_FBITS = 32 - _QBITS              # position inside a bin
+_EDGES = {}                       # device -> fp32 bin edges of N(0,1), [2^20 + 1]
+
+
+def _normal_edges(device) -> torch.Tensor:
+    key = str(torch.device(device))
+    if key not in _EDGES:
+        if "cpu" not in _EDGES:
+            import numpy as np
+            from scipy.special import ndtri
+            n = 1 << _QBITS
+            u = np.arange(n + 1, dtype=np.float64) / n
+            u[0], u[n] = 0.25 / n, 1.0 - 0.25 / n      # finite outer edges, symmetric
+            e = ndtri(u)
+            e[n // 2:] = -e[n // 2::-1][:n // 2 + 1]   # exact antisymmetry before rounding
+            _EDGES["cpu"] = torch.from_numpy(e.astype(np.float32))
+        _EDGES[key] = _EDGES["cpu"].to(device)
+    return _EDGES[key]
 
 
 def draw(seed: int, tensor_id: int, index: torch.Tensor, dtype=torch.bfloat16) -> torch.Tensor:
     """Values at flat element indices ``index`` (int64, < 2^32) of one tensor."""
     k1 = _lowbias32_int(seed * 8 + tensor_id * 2 + 1)
-    k2 = _lowbias32_int(seed * 8 + tensor_id * 2 + 2)
-    h1 = _lowbias32(_lowbias32(index) ^ k1)
-    h2 = _lowbias32(h1 ^ k2)
-    s = (h1 & 0xFFFF) + (h1 >> 16) + (h2 & 0xFFFF) + (h2 >> 16) - 131070
-    x = s.to(torch.float32) * torch.tensor(_IH4_SCALE, dtype=torch.float32, device=s.device)
+    h = _lowbias32(_lowbias32(index) ^ k1)
+    edges = _normal_edges(index.device)
+    b = h >> _FBITS
+    e0, e1 = edges[b], edges[b + 1]
+    w = ((h & ((1 << _FBITS) - 1)) * 2 + 1).to(torch.float32) * (2.0 ** -(_FBITS + 1))   # exact
+    step = (e1 - e0) * w            # one rounding
+    x = e0 + step                   # one rounding
     return x.to(dtype)
 
 

@@ -149,3 +149,15 @@ def test_video_segment_dq_budget():
               f"p99.9 {tails[n]:.2e}")
     assert tails[18] > 1e-2          # small samples do reach the values seen on the GPU
     assert tails[18] <= 2e-2 and tails[64] <= 1.2e-2
+    # The largest element error against max|ref| as the scale: taken over these 256 rows it stays well
+    # inside 2e-2; taken over a two-dozen-row sample, whose max|ref| can miss the segment's large
+    # entries, it spreads up to about 2% (which is why the full-size test pools a segment's sampled
+    # rows over all heads before taking the scale).
+    err = np.abs(e2e - exact).max(axis=1)
+    scale_all = max(1.0, np.abs(exact).max())
+    assert err.max() / scale_all <= 1e-2
+    ratios = []
+    for sub in (pick.choice(len(rows), size=24, replace=False) for _ in range(2000)):
+        ratios.append(err[sub].max() / max(1.0, np.abs(exact[sub]).max()))
+    print(f"  largest element error / max|ref|: {err.max() / scale_all:.2e} over 256 rows, "
+          f"p99.9 {np.percentile(ratios, 99.9):.2e} over 24-row samples")

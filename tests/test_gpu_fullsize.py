@@ -7,10 +7,10 @@ backward), checked on seeded samples the fp64 oracle computes one by one:
     tile edges (rows 63/64, 127/128, 255/256, 511/512) and seeded rows; a
     shard row is checked per block (partial O_b, LSE_b) and after the merge
     against attention over the concatenation of its blocks.  Output and LSE
-    and dQ's max abs error are checked per head; dQ's relative Frobenius error
-    over the sampled rows of all heads of a segment together (a handful of
-    rows of a nearly one-hot segment would make that ratio swing with the
-    sample, see tests/test_bwd_error_budget.py);
+    are checked per head; dQ's max abs error and relative Frobenius error
+    over the sampled rows of all heads of a segment together (the scale
+    max|ref| and the Frobenius ratio of a handful of rows of a nearly one-hot
+    segment swing with the sample, see tests/test_bwd_error_budget.py);
   * dK and dV on sampled keys of one seeded head, which needs the oracle's O
     and LSE for every query of the segment; for the 31,110 x 497,760 shard
     this is too slow on the host, so there it is replaced by identities that
@@ -137,9 +137,7 @@ def test_full_size_sampled_parity(name):
             np.testing.assert_allclose(to64(res["lse"][idx, h]), l, rtol=0, atol=LSE_TOL)
             # dQ of the sampled rows (needs only those rows' statistics)
             g_q, _, _ = oracle.attend_bwd(qr, kk, vv, dor, scale, k_rows=np.array([], dtype=np.int64))
-            got_q = to64(res["dq"][idx, h])
-            _bwd_maxabs(got_q, g_q, f"{name} seg {s} head {h} dq")
-            dq_got.append(got_q)
+            dq_got.append(to64(res["dq"][idx, h]))
             dq_ref.append(g_q)
             # dK/dV of sampled keys: every query of the segment, one head
             if h == dkdv_head and (not shard or plan["shard_dkdv"]):
@@ -152,7 +150,11 @@ def test_full_size_sampled_parity(name):
                 for got, ref, nm in ((to64(res["dk"][kp, h]), g_k, "dk"), (to64(res["dv"][kp, h]), g_v, "dv")):
                     _bwd_maxabs(got, ref, f"{name} seg {s} head {h} {nm}")
                     _bwd_fro(got, ref, f"{name} seg {s} head {h} {nm}")
-        _bwd_fro(np.concatenate(dq_got), np.concatenate(dq_ref), f"{name} seg {s} all heads dq")
+        # dQ of the segment, all heads' sampled rows together: the max-abs bound takes its scale from the
+        # whole sample (one head's two dozen rows of a nearly one-hot segment can miss its large entries)
+        dq_got, dq_ref = np.concatenate(dq_got), np.concatenate(dq_ref)
+        _bwd_maxabs(dq_got, dq_ref, f"{name} seg {s} all heads dq")
+        _bwd_fro(dq_got, dq_ref, f"{name} seg {s} all heads dq")
         # identities that hold at any size, every head: sum_j dK_j = 0, sum_j dV_j = sum_i dO_i
         dk_sum = res["dk"][kidx].double().sum(0)
         dk_abs = res["dk"][kidx].double().abs().sum(0)

@@ -1,6 +1,7 @@
 """Shapes and generator properties of the synthetic workloads."""
 import os
 
+import numpy as np
 import torch
 
 from paper_2608_01150_amd import workloads as W
@@ -54,3 +55,26 @@ def test_scaled_segment_is_exactly_times_four():
                                                       (a + 2) * w.num_heads * w.head_dim), torch.bfloat16)
     got = w.slice(W.TENSOR_Q, a, a + 2).reshape(-1)
     assert torch.equal(got, plain * 4)
+
+
+def test_draw_follows_the_standard_normal():
+    """The quantile-table generator against N(0,1): moments, tail fractions at 2, 3 and 4 sigma,
+    the Kolmogorov-Smirnov distance on 2^21 fp32 draws, the sign symmetry of its table, and the
+    bound of about 5.06 sigma set by the quarter-bin outer edges."""
+    from scipy.special import ndtr, ndtri
+    n = 1 << 21
+    x = W.draw(7, 0, torch.arange(n, dtype=torch.int64), dtype=torch.float32).double().numpy()
+    assert abs(x.mean()) < 3e-3 and abs(x.std() - 1) < 3e-3
+    assert abs(((x - x.mean()) ** 4).mean() / x.var() ** 2 - 3) < 0.03
+    for t in (2.0, 3.0, 4.0):
+        want = 2 * ndtr(-t)
+        got = (np.abs(x) > t).mean()
+        assert abs(got - want) < 5 * np.sqrt(want / n), (t, got, want)
+    xs = np.sort(x)
+    cdf = ndtr(xs)
+    ks = max((np.arange(1, n + 1) / n - cdf).max(), (cdf - np.arange(n) / n).max())
+    assert ks < 1.63 / np.sqrt(n)          # 1% level of the KS test
+    e = W._normal_edges("cpu").double().numpy()
+    assert np.array_equal(e, -e[::-1])
+    assert e[-1] == np.float32(ndtri(1 - 0.25 / (1 << W._QBITS)))
+    assert np.abs(x).max() <= e[-1] and 5.0 < e[-1] < 5.1
