@@ -309,9 +309,14 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       if (m + PFC < NP) cring[m % PFC] = c_op(m + PFC);
       // Block 0's PV MFMAs carry block 1's exponentials; block 1's sum is
       // checked before its own PV MFMAs.
+      // Each packed word is pinned here too: otherwise the compiler sinks the
+      // conversions past the sum check, in front of block 1's first PV MFMA.
       if (m < NP / 2) {
 #pragma unroll
-        for (int c = m * 8 / (NP / 2); c < (m + 1) * 8 / (NP / 2); ++c) expo(1, c);
+        for (int c = m * 8 / (NP / 2); c < (m + 1) * 8 / (NP / 2); ++c) {
+          expo(1, c);
+          asm volatile("" : "+v"(pb[1][c >> 2][c & 3]), "+v"(lsum[1]));
+        }
       }
       if (m == NP / 2) block_done(1);
       const int kb = m / (NP / 2), db = (m % (NP / 2)) >> 1, s2 = m & 1;
