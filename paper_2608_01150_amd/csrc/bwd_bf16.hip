@@ -21,7 +21,7 @@
 //                    dQ^T += K^T dS^T                 MFMA
 //                  A shard row sums its blocks inside one item.
 // Q/dO (dK/dV) and K/V (dQ) tiles are staged row-major (padded pitch,
-// conflict-free) in three LDS buffers by direct buffer-to-LDS loads issued
+// conflict-free) in rotating LDS buffers by direct buffer-to-LDS loads issued
 // ahead of use; the transposed operands (Q^T, dO^T, K^T) come straight from
 // the row-major tiles through LDS transpose reads.
 
@@ -350,20 +350,22 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdParams p) 
 // to 256 query rows of one head.  A segment's K/V ranges are consecutive rows
 // of K and V, and dQ sums over all of them against the final LSE, so the item
 // streams the segment's keys [k_start, k_start + k_len) as one range: block
-// boundaries play no part in the backward.  64-key K/V tiles rotate through
-// three LDS buffers, fetched two steps ahead (waves 0-3 load K, 4-7 load V,
-// each fetch's instructions spread over a step's S/dP MFMAs).
+// boundaries play no part in the backward.  128-key K/V tiles rotate through
+// two LDS buffers, fetched one tile ahead (waves 0-3 load K, 4-7 load V, each
+// fetch's instructions spread over the S/dP MFMAs); a tile is two 64-key
+// steps and one barrier.
 constexpr int kDqThreads = 512;
 
 template <int D>
 __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
   constexpr int BN = kDqTileN;                  // 64 keys per step
+  constexpr int TN = 2 * BN;                    // keys per staged tile: two steps per barrier
   constexpr int PITCH = Pad<D>::PITCH;
-  constexpr int TILE = BN * PITCH;
-  using Dma = TileDma<D, BN>;
-  constexpr int DMA_PER_FETCH = Dma::PER_WAVE;  // per wave and fetch (four waves share a tile)
-  // Three buffers of each tile as separate objects (see the forward kernel).
-  __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], ks2[TILE], vs0[TILE], vs1[TILE], vs2[TILE];
+  constexpr int TILE = TN * PITCH;
+  using Dma = TileDma<D, BN>;                   // one 64-key half of a staged tile
+  constexpr int DMA_PER_STEP = Dma::PER_WAVE;   // per wave and half (four waves share a tile)
+  // Two buffers of each tile as separate objects (see the forward kernel).
+  __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], vs0[TILE], vs1[TILE];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -410,15 +412,21 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
   Dma dma;
   dma.init(wave & 3, lane, row_bytes);
   auto fetch = [&](int kt, char* kdst, char* vdst) {
-    dma.issue(loads_k ? kdst : vdst, src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
+    char* dst = loads_k ? kdst : vdst;
+    dma.issue(dst, src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
+    dma.issue(dst + BN * PITCH, src0 + (int64_t)(kt + BN) * rs, it.k_len - kt - BN, row_bytes);
   };
-  // Inside the loop a fetch is only set up here; the next step's S/dP MFMAs
-  // issue its instructions one at a time (as in the forward kernel).
-  i32x4 next_rsrc;
-  uint32_t next_lds;
+  // Inside the loop a fetch is only set up here; the S/dP MFMAs of the tile's
+  // two steps issue its instructions one at a time, one half each.
+  i32x4 next_rsrc[2];
+  uint32_t next_lds[2];
   auto fetch_spread = [&](int kt, char* kdst, char* vdst) {
-    next_rsrc = Dma::resource(src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
-    next_lds = lds_addr(loads_k ? kdst : vdst);
+    char* dst = loads_k ? kdst : vdst;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      next_rsrc[h] = Dma::resource(src0 + (int64_t)(kt + h * BN) * rs, it.k_len - kt - h * BN, row_bytes);
+      next_lds[h] = lds_addr(dst + h * BN * PITCH);
+    }
   };
 
   // One 64-key step as two 32-key blocks kb, software-pipelined inside the
@@ -426,7 +434,8 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
   //   S/dP MFMAs of kb 0; S/dP MFMAs of kb 1 with the softmax of kb 0;
   //   dQ MFMAs of kb 0 with the softmax of kb 1; dQ MFMAs of kb 1.
   // A operands come from LDS through a ring of loads issued PF MFMAs ahead.
-  auto step = [&](const char* kbuf, const char* vbuf) __attribute__((always_inline)) {
+  // half: which of the tile's two steps (0 or 1, a literal at the call sites).
+  auto step = [&](const char* kbuf, const char* vbuf, int half) __attribute__((always_inline)) {
     const char* ka = kbuf + a_off;
     const char* va = vbuf + a_off;
     const char* kt_ = kbuf + t_off;
@@ -442,8 +451,8 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
       return tr_operand<D>(kt_, (m / (NQ / 2)) * 32 + 16 * (m & 1), ((m % (NQ / 2)) >> 1) * 32);
     };
     constexpr int PF = 6, PFC = 3;
-    constexpr int DMA_GAP = NSD / DMA_PER_FETCH;  // S/dP MFMAs between the spread fetch's instructions
-    static_assert(DMA_GAP >= 2 && (DMA_PER_FETCH - 1) * DMA_GAP + 1 < NSD, "spread fetch must fit the S/dP MFMAs");
+    constexpr int DMA_GAP = NSD / DMA_PER_STEP;  // S/dP MFMAs between the spread fetch's instructions
+    static_assert(DMA_GAP >= 2 && (DMA_PER_STEP - 1) * DMA_GAP + 1 < NSD, "spread fetch must fit the S/dP MFMAs");
     // register i <-> key kb*32 + 16*(i/8) + 8g + i%8 of this tile, query = lane's row.
     // P is clamped to [0, 1] (exact: every true P is at most 1), a free
     // modifier of the exp.  That keeps dS finite for the keys past the
@@ -475,7 +484,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
         dpc[kb] = mfma32(a, of[kk], kk == 0 ? negd : dpc[kb]);
       else
         sc[kb] = mfma32(a, qf[kk], sc[kb]);
-      if (j % DMA_GAP == 1 && j / DMA_GAP < DMA_PER_FETCH) dma.issue_one(next_rsrc, next_lds, j / DMA_GAP);
+      if (j % DMA_GAP == 1 && j / DMA_GAP < DMA_PER_STEP) dma.issue_one(next_rsrc[half], next_lds[half], j / DMA_GAP);
       // kb 1's MFMAs carry kb 0's softmax: 16 elements over NSD/2 MFMAs.
       if (j >= NSD / 2 && ((j - NSD / 2) % (NSD / 16)) == NSD / 16 - 1) softmax2(0, 2 * ((j - NSD / 2) / (NSD / 16)));
       __builtin_amdgcn_sched_barrier(0);
@@ -501,37 +510,37 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
 
   // Waves with no query rows skip the math (see the forward kernel).
   const bool wave_live = wave * 32 < it.q_len;
-  auto run = [&](const char* kbuf, const char* vbuf) __attribute__((always_inline)) {
+  auto run = [&](const char* kbuf, const char* vbuf, int half) __attribute__((always_inline)) {
     if (wave_live) {
-      step(kbuf, vbuf);
+      step(kbuf, vbuf, half);
     } else {
 #pragma unroll
-      for (int jj = 0; jj < DMA_PER_FETCH; ++jj) dma.issue_one(next_rsrc, next_lds, jj);
+      for (int jj = 0; jj < DMA_PER_STEP; ++jj) dma.issue_one(next_rsrc[half], next_lds[half], jj);
     }
   };
+  // One staged tile as two steps with no barrier between them (see the
+  // forward kernel); keys past the range add zero, so a tile whose second
+  // half lies past the range skips that step.
+  auto tile = [&](const char* kbuf, const char* vbuf, int kt) __attribute__((always_inline)) {
+    run(kbuf, vbuf, 0);
+    if (kt + BN < it.k_len) run(kbuf + BN * PITCH, vbuf + BN * PITCH, 1);
+  };
 
-  // Three buffer sets in rotation, unrolled by three, as in the forward.
+  // Two buffer sets in rotation, unrolled by two, as in the forward.
   if (it.k_len > 0) {
     fetch(0, ks0, vs0);
-    fetch(BN, ks1, vs1);
     for (int kt = 0;;) {
-      wait_vmem_keep<DMA_PER_FETCH>();
-      __syncthreads();  // tile in buffers 0 complete; buffers 2 no longer read
-      fetch_spread(kt + 2 * BN, ks2, vs2);
-      run(ks0, vs0);
-      kt += BN;
+      wait_vmem();
+      __syncthreads();  // tile in buffers 0 complete; buffers 1 no longer read
+      fetch_spread(kt + TN, ks1, vs1);
+      tile(ks0, vs0, kt);
+      kt += TN;
       if (kt >= it.k_len) break;
-      wait_vmem_keep<DMA_PER_FETCH>();
+      wait_vmem();
       __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
-      fetch_spread(kt + 2 * BN, ks0, vs0);
-      run(ks1, vs1);
-      kt += BN;
-      if (kt >= it.k_len) break;
-      wait_vmem_keep<DMA_PER_FETCH>();
-      __syncthreads();  // tile in buffers 2 complete; buffers 1 no longer read
-      fetch_spread(kt + 2 * BN, ks1, vs1);
-      run(ks2, vs2);
-      kt += BN;
+      fetch_spread(kt + TN, ks0, vs0);
+      tile(ks1, vs1, kt);
+      kt += TN;
       if (kt >= it.k_len) break;
     }
     wait_vmem();  // the lookahead loads must land before the workgroup's LDS is released

@@ -10,12 +10,13 @@
 //                        straight from registers (B)
 // Computing the transposed products keeps one query per lane, so the row max
 // needs a single cross-lane exchange (lanes l and l^32) and the softmax
-// output is already the B operand of the next MFMA.  K and V tiles are staged
-// row-major (padded pitch, conflict-free) in three LDS buffers by direct
-// global-to-LDS loads issued two steps ahead (waves 0-3 load K, waves 4-7
-// load V, each fetch's instructions spread over a step's S MFMAs), one
-// barrier per step.  A staged tile serves 256 queries, so the
-// staging costs half as much per MFMA as with 128-row items.
+// output is already the B operand of the next MFMA.  K and V are staged
+// row-major (padded pitch, conflict-free) in 128-key tiles, two LDS buffers
+// of each, by direct global-to-LDS loads issued one tile ahead (waves 0-3
+// load K, waves 4-7 load V, each fetch's instructions spread over the S
+// MFMAs); a tile is two 64-key steps and one barrier.  A staged tile serves
+// 256 queries, so the staging costs half as much per MFMA as with 128-row
+// items.
 //
 // Epilogue: WHOLE items write the final bf16 output and the LSE; SHARD items
 // write the block-normalised partial (fp32, or bf16 on request) and its LSE
@@ -135,13 +136,16 @@ __device__ __forceinline__ void fwd_store(const FwdParams& p, const Item& it, in
 template <int D>
 __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
   constexpr int PITCH = Pad<D>::PITCH;
-  constexpr int TILE = BN * PITCH;
+  constexpr int TN = 2 * BN;  // keys per staged tile: two steps per barrier
+  constexpr int TILE = TN * PITCH;
+  // A staged tile is loaded as two 64-key halves with the same per-lane
+  // offsets; per wave DMA_PER_STEP direct-to-LDS instructions per half (four
+  // waves share a tile), the next tile's half h issued during step h.
   using Dma = TileDma<D, BN>;
-  // Per-wave direct-to-LDS instructions of one fetch (four waves share a tile).
-  constexpr int DMA_PER_FETCH = Dma::PER_WAVE;
-  // Three buffers of each tile as separate objects, so the compiler can tell
+  constexpr int DMA_PER_STEP = Dma::PER_WAVE;
+  // Two buffers of each tile as separate objects, so the compiler can tell
   // the direct-to-LDS loads filling one buffer from the reads of another.
-  __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], ks2[TILE], vs0[TILE], vs1[TILE], vs2[TILE];
+  __shared__ __attribute__((aligned(16))) char ks0[TILE], ks1[TILE], vs0[TILE], vs1[TILE];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -183,16 +187,21 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
   Dma dma;
   dma.init(wave & 3, lane, row_bytes);
   auto fetch = [&](int kt, char* kdst, char* vdst) {
-    dma.issue(loads_k ? kdst : vdst, src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
+    char* dst = loads_k ? kdst : vdst;
+    dma.issue(dst, src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
+    dma.issue(dst + BN * PITCH, src0 + (int64_t)(kt + BN) * rs, it.k_len - kt - BN, row_bytes);
   };
-  // Inside the loop a fetch is only set up here; the next step's S MFMAs
-  // issue its DMA_PER_FETCH instructions one at a time (all of them before
-  // the step ends, so the wait before the next barrier is unchanged).
-  i32x4 next_rsrc;
-  uint32_t next_lds;
+  // Inside the loop a fetch is only set up here; the S MFMAs of the tile's
+  // two steps issue its instructions one at a time, one half each.
+  i32x4 next_rsrc[2];
+  uint32_t next_lds[2];
   auto fetch_spread = [&](int kt, char* kdst, char* vdst) {
-    next_rsrc = Dma::resource(src0 + (int64_t)kt * rs, it.k_len - kt, row_bytes);
-    next_lds = lds_addr(loads_k ? kdst : vdst);
+    char* dst = loads_k ? kdst : vdst;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      next_rsrc[h] = Dma::resource(src0 + (int64_t)(kt + h * BN) * rs, it.k_len - kt - h * BN, row_bytes);
+      next_lds[h] = lds_addr(dst + h * BN * PITCH);
+    }
   };
 
   // One 64-key step as two 32-key blocks kb, each its own online-softmax
@@ -201,14 +210,15 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
   //   S of kb 0;  S of kb 1 with the softmax of kb 0;  max/rescale of kb 1;
   //   PV of kb 0 with the exponentials of kb 1;  PV of kb 1.
   // A operands come from LDS through rings of loads issued ahead of use.
-  auto step = [&](const char* kbuf, const char* vbuf, int kt) __attribute__((always_inline)) {
+  // half: which of the tile's two steps (0 or 1, a literal at the call sites).
+  auto step = [&](const char* kbuf, const char* vbuf, int kt, int half) __attribute__((always_inline)) {
     const char* ka = kbuf + a_off;
     const char* vt = vbuf + t_off;
     constexpr int NS = 2 * (D / 16);        // S MFMAs per step
     constexpr int NP = 2 * (D / 32) * 2;    // PV MFMAs per step
     constexpr int PF = 6, PFC = 3;
-    constexpr int DMA_GAP = NS / DMA_PER_FETCH;  // S MFMAs between the spread fetch's instructions
-    static_assert(DMA_GAP >= 2 && (DMA_PER_FETCH - 1) * DMA_GAP + 1 < NS, "spread fetch must fit the S MFMAs");
+    constexpr int DMA_GAP = NS / DMA_PER_STEP;  // S MFMAs between the spread fetch's instructions
+    static_assert(DMA_GAP >= 2 && (DMA_PER_STEP - 1) * DMA_GAP + 1 < NS, "spread fetch must fit the S MFMAs");
     // S operand j: keys of block j/(NS/2) (rows perm32), d chunk j%(NS/2).
     auto a_op = [&](int j) {
       return *reinterpret_cast<const u32x4*>(ka + poff<D>((j / (NS / 2)) * 32, (j % (NS / 2)) * 16));
@@ -279,7 +289,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       if (j + PF < NS) ring[j % PF] = a_op(j + PF);
       const int kb = j / (NS / 2);
       s[kb] = mfma32(a, qf[j % (NS / 2)], s[kb]);
-      if (j % DMA_GAP == 1 && j / DMA_GAP < DMA_PER_FETCH) dma.issue_one(next_rsrc, next_lds, j / DMA_GAP);
+      if (j % DMA_GAP == 1 && j / DMA_GAP < DMA_PER_STEP) dma.issue_one(next_rsrc[half], next_lds[half], j / DMA_GAP);
       // Block 1's MFMAs carry block 0's softmax: the mask of a partial tile
       // first, then the eight exponential pairs spread over the remaining
       // slots.  Each packed word and the block's sum are pinned where they are
@@ -331,42 +341,42 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
   // loads, which the other waves need; the SIMD's other wave then has the
   // matrix core to itself.
   const bool wave_live = wave * 32 < it.q_len;
-  auto run = [&](const char* kbuf, const char* vbuf, int kt) __attribute__((always_inline)) {
+  auto run = [&](const char* kbuf, const char* vbuf, int kt, int half) __attribute__((always_inline)) {
     if (wave_live) {
-      step(kbuf, vbuf, kt);
+      step(kbuf, vbuf, kt, half);
     } else {
 #pragma unroll
-      for (int jj = 0; jj < DMA_PER_FETCH; ++jj) dma.issue_one(next_rsrc, next_lds, jj);
+      for (int jj = 0; jj < DMA_PER_STEP; ++jj) dma.issue_one(next_rsrc[half], next_lds[half], jj);
     }
   };
+  // One staged tile of TN keys as two steps, with no barrier between them;
+  // a tile whose second half lies past the range runs only its first step
+  // (the loop ends there, so the fetch that step would finish is not needed).
+  auto tile = [&](const char* kbuf, const char* vbuf, int kt) __attribute__((always_inline)) {
+    run(kbuf, vbuf, kt, 0);
+    if (kt + BN < it.k_len) run(kbuf + BN * PITCH, vbuf + BN * PITCH, kt + BN, 1);
+  };
 
-  // Three buffer sets in rotation, the loop unrolled by three.  Tile t+2 is
-  // fetched during step t, after the barrier that retires tile t-1's buffers, so every
-  // tile has two steps to arrive; fetches past the range read zero (an empty
-  // resource) and are never used.  Before the barrier a wave waits only for its own loads of
-  // tile t: the DMA_PER_FETCH loads of tile t+1 it issued later may stay in
-  // flight.
+  // Two buffer sets in rotation, the loop unrolled by two.  Tile t+1 is
+  // fetched during tile t, after the barrier that retires tile t-1's buffers;
+  // a fetch past the range reads zero (an empty resource) and is never used.
+  // Before the barrier a wave waits for all of its loads: only tile t+1's
+  // are outstanding.  Two 64-key steps per barrier halve the barriers of a
+  // 64-key tile rotation at the same prefetch distance in time.
   if (it.k_len > 0) {
     fetch(0, ks0, vs0);
-    fetch(BN, ks1, vs1);
     for (int kt = 0;;) {
-      wait_vmem_keep<DMA_PER_FETCH>();
-      __syncthreads();  // tile in buffers 0 complete; buffers 2 no longer read
-      fetch_spread(kt + 2 * BN, ks2, vs2);
-      run(ks0, vs0, kt);
-      kt += BN;
+      wait_vmem();
+      __syncthreads();  // tile in buffers 0 complete; buffers 1 no longer read
+      fetch_spread(kt + TN, ks1, vs1);
+      tile(ks0, vs0, kt);
+      kt += TN;
       if (kt >= it.k_len) break;
-      wait_vmem_keep<DMA_PER_FETCH>();
+      wait_vmem();
       __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
-      fetch_spread(kt + 2 * BN, ks0, vs0);
-      run(ks1, vs1, kt);
-      kt += BN;
-      if (kt >= it.k_len) break;
-      wait_vmem_keep<DMA_PER_FETCH>();
-      __syncthreads();  // tile in buffers 2 complete; buffers 1 no longer read
-      fetch_spread(kt + 2 * BN, ks1, vs1);
-      run(ks2, vs2, kt);
-      kt += BN;
+      fetch_spread(kt + TN, ks0, vs0);
+      tile(ks1, vs1, kt);
+      kt += TN;
       if (kt >= it.k_len) break;
     }
     wait_vmem();  // the lookahead loads must land before the workgroup's LDS is released
