@@ -45,12 +45,17 @@ constexpr float kSumBound = 0x1p64f;
 // Epilogue of a forward item: normalises the running output of this lane's
 // query and stores it by the item's kind.  o[db][i] is (d = db*32 +
 // 16*(i/8) + 8*g + i%8, query qr); m_run is the running maximum (log2
-// units) and l_part this lane's half of the row sum.
+// units), l_part this lane's half of the row sum of the exponentials and
+// l_rnd its half of the sum of the same values rounded to bf16, as they
+// entered O += P V.  The output is normalised by the rounded sum, so its
+// weights sum to one exactly: the rounding of a dominant P (any value in
+// [1, 2^64) against a running maximum that a later key exceeds) cancels
+// instead of scaling the output.  The LSE takes the unrounded sum.
 template <int D>
 __device__ __forceinline__ void fwd_store(const FwdParams& p, const Item& it, int qr, bool q_ok, int g,
-                                          const f32x16 (&o)[D / 32], float m_run, float l_part) {
-  const float l = xor32_sum(l_part);
-  const float inv = l > 0.f ? 1.f / l : 0.f;
+                                          const f32x16 (&o)[D / 32], float m_run, float l_part, float l_rnd) {
+  const float l = xor32_sum(l_part), lr = xor32_sum(l_rnd);
+  const float inv = lr > 0.f ? 1.f / lr : 0.f;
   const float lse = l > 0.f ? (m_run + __log2f(l)) * kLn2 : -INFINITY;
   if (!q_ok) return;
   const int64_t row = (int64_t)(it.q_start + qr) * p.num_heads + it.head;
@@ -169,7 +174,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
   // vmcnt wait there (which would also drain the in-flight tile DMAs).
   __builtin_amdgcn_s_waitcnt(0);
 
-  float m_run = kNegBig, l_part = 0.f;
+  float m_run = kNegBig, l_part = 0.f, l_rnd = 0.f;
   f32x16 o[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) o[db] = f32x16{};
@@ -231,7 +236,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     // s[kb][i] is the raw score of (key kb*32 + 16*(i/8) + 8*g + i%8, query qr).
     f32x16 s[2];
     u32x4 pb[2][2];
-    float lsum[2] = {0.f, 0.f};
+    float lsum[2] = {0.f, 0.f}, lrnd[2] = {0.f, 0.f};
     // Keys past the range on a partial tile: score -inf, exact at any positive scale.
     auto mask = [&](int kb) {
       if (nvalid < BN) {
@@ -248,6 +253,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       const float e1 = fast_exp2(fmaf(s[kb][2 * c + 1], p.scale_log2, -m_run));
       lsum[kb] += e0 + e1;
       pb[kb][c >> 2][c & 3] = pack_bf16(e0, e1);
+      lrnd[kb] = sum_bf16x2(pb[kb][c >> 2][c & 3], lrnd[kb]);
     };
     // The slow path of block kb (see kSumBound): when it is taken for block 1,
     // block 0 has entered O already, and the rescale covers it there.
@@ -260,18 +266,20 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       const float alpha = fast_exp2(m_run - m_new);
       m_run = m_new;
       l_part *= alpha;
+      l_rnd *= alpha;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
       }
-      lsum[kb] = 0.f;
+      lsum[kb] = lrnd[kb] = 0.f;
 #pragma unroll
       for (int c = 0; c < 8; ++c) expo(kb, c);
     };
     auto block_done = [&](int kb) {
       if (__any(lsum[kb] > kSumBound)) block_fix(kb);
       l_part += lsum[kb];
+      l_rnd += lrnd[kb];
     };
 
     u32x4 ring[PF];
@@ -302,7 +310,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
         for (int c = c0; c < c1; ++c) {
           expo(0, c);
-          asm volatile("" : "+v"(pb[0][c >> 2][c & 3]), "+v"(lsum[0]));
+          asm volatile("" : "+v"(pb[0][c >> 2][c & 3]), "+v"(lsum[0]), "+v"(lrnd[0]));
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -325,7 +333,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
         for (int c = m * 8 / (NP / 2); c < (m + 1) * 8 / (NP / 2); ++c) {
           expo(1, c);
-          asm volatile("" : "+v"(pb[1][c >> 2][c & 3]), "+v"(lsum[1]));
+          asm volatile("" : "+v"(pb[1][c >> 2][c & 3]), "+v"(lsum[1]), "+v"(lrnd[1]));
         }
       }
       if (m == NP / 2) block_done(1);
@@ -382,7 +390,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     wait_vmem();  // the lookahead loads must land before the workgroup's LDS is released
   }
 
-  fwd_store<D>(p, it, qr, q_ok, g, o, m_run, l_part);
+  fwd_store<D>(p, it, qr, q_ok, g, o, m_run, l_part, l_rnd);
 }
 
 }  // namespace

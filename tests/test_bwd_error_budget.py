@@ -6,8 +6,9 @@ roundings, each emulated here with numpy on top of the oracle's definitions
 
   O storage     the forward's output is stored as bf16, and D_i = dO_i . O_i
                 reads it back;
-  forward P     the forward rounds each P_ij to bf16 before O += P V (its row
-                sum l stays fp32), so the stored O carries that error too;
+  forward P     the forward rounds each P_ij to bf16 before O += P V and
+                normalises by the sum of the rounded values (the LSE takes
+                the unrounded sum), so the stored O carries that error too;
   backward P/dS the backward rounds P_ij (for dV) and dS_ij (for dK, dQ) to
                 bf16 before the MFMAs, and stores dQ, dK, dV as bf16.
 
@@ -44,13 +45,14 @@ def rel(a, b):
 
 
 def forward_emulated(q, k, v, scale):
-    """O as the bf16 forward stores it: P rounded to bf16 in the P V product, the row sum in full
-    precision, the result rounded to bf16; LSE rounded to fp32."""
+    """O as the bf16 forward stores it: P rounded to bf16 in the P V product and in the row sum that
+    normalises it, the result rounded to bf16; LSE from the unrounded row sum, rounded to fp32."""
     s = scale * (q @ k.T)
     m = s.max(axis=1, keepdims=True)
     p = np.exp(s - m)
     l = p.sum(axis=1, keepdims=True)
-    o = bf16((bf16(p) @ v) / l)
+    pb = bf16(p)
+    o = bf16((pb @ v) / pb.sum(axis=1, keepdims=True))
     lse = fp32(m[:, 0] + np.log(l[:, 0]))
     return o, lse
 

@@ -2,20 +2,22 @@
 bench.py times (one forward over the whole packed batch, the LSE merge, the
 backward), checked on seeded samples the fp64 oracle computes one by one:
 
-  * forward and dQ on sampled query rows of sampled segments, on EVERY head:
-    the first and last rows, both sides of the 64-, 128-, 256- and 512-row
-    tile edges (rows 63/64, 127/128, 255/256, 511/512) and seeded rows; a
-    shard row is checked per block (partial O_b, LSE_b) and after the merge
-    against attention over the concatenation of its blocks.  Output and LSE
-    are checked per head; dQ's max abs error and relative Frobenius error
+  * forward and dQ on 64 sampled query rows of sampled segments, on EVERY
+    head: the first and last rows, both sides of the 64-, 128-, 256- and
+    512-row tile edges (rows 63/64, 127/128, 255/256, 511/512) and seeded
+    rows; a shard row is checked per block (partial O_b, LSE_b) and after the
+    merge against attention over the concatenation of its blocks.  Output and
+    LSE are checked per head; dQ's max abs error and relative Frobenius error
     over the sampled rows of all heads of a segment together (the scale
     max|ref| and the Frobenius ratio of a handful of rows of a nearly one-hot
     segment swing with the sample, see tests/test_bwd_error_budget.py);
-  * dK and dV on sampled keys of one seeded head, which needs the oracle's O
-    and LSE for every query of the segment; for the 31,110 x 497,760 shard
-    this is too slow on the host, so there it is replaced by identities that
-    hold at any size (sum over all keys of dK = 0, sum over all keys of dV =
-    sum over queries of dO) checked on every head.
+  * on one seeded head, EVERY query row of the segment (output, LSE, per-block
+    partials of a shard, dQ) and dK, dV on sampled keys, which need the
+    oracle's O and LSE for every query of the segment anyway; for the
+    31,110 x 497,760 shard this is too slow on the host, so there it is
+    replaced by identities that hold at any size (sum over all keys of dK =
+    0, sum over all keys of dV = sum over queries of dO) checked on every
+    head.
 
 Inputs come from the seeded counter-based generator, drawn on the GPU (by
 torch, not by the library) for the launch.  The oracle reads those same
@@ -75,7 +77,7 @@ def _ranges(w, s):
             for j in range(w.kv_first[s], w.kv_first[s] + w.kv_count[s])]
 
 
-def _rows(rng, a, b, extra=14):
+def _rows(rng, a, b, extra=54):
     n = b - a
     base = {min(n - 1, e) for e in EDGES} | {n - 1}
     base |= set(rng.choice(n, size=min(n, extra), replace=False).tolist())
@@ -139,13 +141,25 @@ def test_full_size_sampled_parity(name):
             g_q, _, _ = oracle.attend_bwd(qr, kk, vv, dor, scale, k_rows=np.array([], dtype=np.int64))
             dq_got.append(to64(res["dq"][idx, h]))
             dq_ref.append(g_q)
-            # dK/dV of sampled keys: every query of the segment, one head
+            # one head, every query of the segment: forward and dQ on all rows,
+            # dK/dV on sampled keys
             if h == dkdv_head and (not shard or plan["shard_dkdv"]):
                 qa = _host(res["q"], slice(a, b), h)
                 doa = _host(res["do"], slice(a, b), h)
+                if shard:
+                    for (k0, k1, b_), kb, vb in zip(rng_, ks, vs):
+                        o_b, l_b = oracle.attend(qa, kb, vb, scale)
+                        np.testing.assert_allclose(to64(res["parts"][0][b_, a:b, h]), o_b, rtol=0, atol=O_TOL)
+                        np.testing.assert_allclose(to64(res["parts"][1][b_, a:b, h]), l_b, rtol=0, atol=LSE_TOL)
+                o_all, l_all = oracle.attend(qa, kk, vv, scale)
+                np.testing.assert_allclose(to64(res["out"][a:b, h]), o_all, rtol=0, atol=O_TOL)
+                np.testing.assert_allclose(to64(res["lse"][a:b, h]), l_all, rtol=0, atol=LSE_TOL)
                 keys = _rows(rng, 0, kk.shape[0], extra=10)
-                _, g_k, g_v = oracle.attend_bwd(qa, kk, vv, doa, scale, q_rows=np.array([], dtype=np.int64),
-                                                k_rows=keys)
+                g_qa, g_k, g_v = oracle.attend_bwd(qa, kk, vv, doa, scale, k_rows=keys)
+                got_qa = to64(res["dq"][a:b, h])
+                _bwd_maxabs(got_qa, g_qa, f"{name} seg {s} head {h} dq, all {b - a} rows")
+                _bwd_fro(got_qa, g_qa, f"{name} seg {s} head {h} dq, all {b - a} rows")
+                print(f"{name} seg {s} head {h}: forward and dQ checked on all {b - a} rows", flush=True)
                 kp = kidx[torch.as_tensor(keys, device="cuda")]
                 for got, ref, nm in ((to64(res["dk"][kp, h]), g_k, "dk"), (to64(res["dv"][kp, h]), g_v, "dv")):
                     _bwd_maxabs(got, ref, f"{name} seg {s} head {h} {nm}")
