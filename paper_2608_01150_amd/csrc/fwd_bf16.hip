@@ -236,7 +236,9 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     // s[kb][i] is the raw score of (key kb*32 + 16*(i/8) + 8*g + i%8, query qr).
     f32x16 s[2];
     u32x4 pb[2][2];
-    float lsum[2] = {0.f, 0.f}, lrnd[2] = {0.f, 0.f};
+    // Each block's two sums in two partial accumulators (words of even and
+    // odd c), which halves their dependency chains.
+    float lsum[2][2] = {}, lrnd[2][2] = {};
     // Keys past the range on a partial tile: score -inf, exact at any positive scale.
     auto mask = [&](int kb) {
       if (nvalid < BN) {
@@ -251,9 +253,9 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     auto expo = [&](int kb, int c) {
       const float e0 = fast_exp2(fmaf(s[kb][2 * c], p.scale_log2, -m_run));
       const float e1 = fast_exp2(fmaf(s[kb][2 * c + 1], p.scale_log2, -m_run));
-      lsum[kb] += e0 + e1;
+      lsum[kb][c & 1] += e0 + e1;
       pb[kb][c >> 2][c & 3] = pack_bf16(e0, e1);
-      lrnd[kb] = sum_bf16x2(pb[kb][c >> 2][c & 3], lrnd[kb]);
+      lrnd[kb][c & 1] = sum_bf16x2(pb[kb][c >> 2][c & 3], lrnd[kb][c & 1]);
     };
     // The slow path of block kb (see kSumBound): when it is taken for block 1,
     // block 0 has entered O already, and the rescale covers it there.
@@ -272,14 +274,14 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
       }
-      lsum[kb] = lrnd[kb] = 0.f;
+      lsum[kb][0] = lsum[kb][1] = lrnd[kb][0] = lrnd[kb][1] = 0.f;
 #pragma unroll
       for (int c = 0; c < 8; ++c) expo(kb, c);
     };
     auto block_done = [&](int kb) {
-      if (__any(lsum[kb] > kSumBound)) block_fix(kb);
-      l_part += lsum[kb];
-      l_rnd += lrnd[kb];
+      if (__any(lsum[kb][0] + lsum[kb][1] > kSumBound)) block_fix(kb);
+      l_part += lsum[kb][0] + lsum[kb][1];
+      l_rnd += lrnd[kb][0] + lrnd[kb][1];
     };
 
     u32x4 ring[PF];
@@ -310,7 +312,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
         for (int c = c0; c < c1; ++c) {
           expo(0, c);
-          asm volatile("" : "+v"(pb[0][c >> 2][c & 3]), "+v"(lsum[0]), "+v"(lrnd[0]));
+          asm volatile("" : "+v"(pb[0][c >> 2][c & 3]), "+v"(lsum[0][c & 1]), "+v"(lrnd[0][c & 1]));
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -333,7 +335,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
         for (int c = m * 8 / (NP / 2); c < (m + 1) * 8 / (NP / 2); ++c) {
           expo(1, c);
-          asm volatile("" : "+v"(pb[1][c >> 2][c & 3]), "+v"(lsum[1]), "+v"(lrnd[1]));
+          asm volatile("" : "+v"(pb[1][c >> 2][c & 3]), "+v"(lsum[1][c & 1]), "+v"(lrnd[1][c & 1]));
         }
       }
       if (m == NP / 2) block_done(1);
