@@ -61,6 +61,7 @@ namespace {
 struct Shape {
   int64_t total_q = 0, total_k = 0;
   bool any_whole_rows = false, any_shard_rows = false;
+  bool multi_block_shard = false;  // a SHARD segment with query rows uses several ranges
   bool ranges_single_owner = true;
 };
 
@@ -125,6 +126,7 @@ zl_status validate_desc(const zl_seg_desc* d, int32_t num_slots_arg, bool check_
       if (lq > 0) sh.any_whole_rows = true;
     } else {
       if (lq > 0) sh.any_shard_rows = true;
+      if (lq > 0 && c > 1) sh.multi_block_shard = true;
       if (step_mode) {
         if (c != 1)
           return fail(ZL_ERR_INVALID_ARG, "ring step: SHARD segment %d must use exactly one range (has %d)", s, c);
@@ -511,14 +513,16 @@ hipError_t timed(int kid, hipStream_t s, F&& launch) {
 
 // Work items per XCD run of the dispatch order (see dispatch_item).  The
 // hardware hands consecutive workgroups to the 8 XCDs in turn, and each XCD
-// has its own L2.  In a launch of WHOLE segments only, a segment's tiles of one
-// head are consecutive in the work table (equal cost, ties by query or key
-// tile) and read the same K/V (or Q/dO) tiles, so runs of 16 keep them on one
-// XCD, where they share that data through its L2.  With SHARD segments the
-// tie-break orders a shard's items by query tile, then block, so plain order
-// (1) already sends block j of every query tile to XCD j mod 8 and the block's
-// K/V stays in one L2; longer runs would mix blocks there.  ZL_XCD_CHUNK (read
-// once, 1..4096) overrides the choice for every launch.
+// has its own L2.  When every segment brings one K/V range (WHOLE segments,
+// and SHARD segments in a ring step or against gathered blocks), a segment's
+// tiles of one head are consecutive in the work table (equal cost, ties by
+// query or key tile) and read the same K/V (or Q/dO) tiles, so runs of 16
+// keep them on one XCD, where they share that data through its L2.  When a
+// SHARD brings several blocks, the tie-break orders its items by query tile,
+// then block, so plain order (1) already sends block j of every query tile to
+// XCD j mod 8 and the block's K/V stays in one L2; longer runs would mix
+// blocks there.  ZL_XCD_CHUNK (read once, 1..4096) overrides the choice for
+// every launch.
 int32_t xcd_chunk(const Shape& sh) {
   static const int32_t env = [] {
     const char* e = std::getenv("ZL_XCD_CHUNK");
@@ -526,7 +530,7 @@ int32_t xcd_chunk(const Shape& sh) {
     return (int32_t)(x >= 1 && x <= 4096 ? x : 0);
   }();
   if (env) return env;
-  return sh.any_shard_rows ? 1 : 16;
+  return sh.multi_block_shard ? 1 : 16;
 }
 
 zl_status hip_status(hipError_t e, const char* what) {
