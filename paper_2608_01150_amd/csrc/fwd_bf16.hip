@@ -210,10 +210,11 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
   };
 
   // One 64-key step as two 32-key blocks kb, each its own online-softmax
-  // update (max, lazy rescale, exponentials), software-pipelined inside the
+  // update (exponentials against the running maximum, the sum check and, in
+  // rare cases, the slow path of kSumBound), software-pipelined inside the
   // wave so that the softmax VALU work runs under MFMAs:
-  //   S of kb 0;  S of kb 1 with the softmax of kb 0;  max/rescale of kb 1;
-  //   PV of kb 0 with the exponentials of kb 1;  PV of kb 1.
+  //   S of kb 0;  S of kb 1 with the softmax of kb 0;  check of kb 0;
+  //   PV of kb 0 with the exponentials of kb 1;  check of kb 1;  PV of kb 1.
   // A operands come from LDS through rings of loads issued ahead of use.
   // half: which of the tile's two steps (0 or 1, a literal at the call sites).
   auto step = [&](const char* kbuf, const char* vbuf, int kt, int half) __attribute__((always_inline)) {
