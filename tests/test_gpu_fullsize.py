@@ -39,6 +39,9 @@ O_TOL, LSE_TOL = 2e-2, 1e-3
 # budget (tests/test_bwd_error_budget.py) puts the chain at 0.24% on unscaled inputs and 0.5-0.6% on the
 # x4-scaled video, with 64-row samples of that video staying under 1.2% (p99.9).
 BWD_REL_FRO = 2e-2
+# Over large samples (every row of a head, or a segment's sampled rows of all heads) the spread is small and
+# the bound is 1e-2: the budget's end-to-end chain on the x4 video is 0.59%, and the GPU measures 0.57% there.
+BWD_REL_FRO_POOLED = 1e-2
 
 # segments checked per workload, and whether dK/dV of the shard is sampled
 PLAN = {
@@ -95,9 +98,9 @@ def _bwd_maxabs(got, ref, name):
     assert err <= bound, f"{name}: max abs err {err} > {bound}"
 
 
-def _bwd_fro(got, ref, name):
+def _bwd_fro(got, ref, name, bound=BWD_REL_FRO):
     rel = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
-    assert rel <= BWD_REL_FRO, f"{name}: relative Frobenius err {rel}"
+    assert rel <= bound, f"{name}: relative Frobenius err {rel}"
     print(f"{name}: rel Frobenius {rel:.3g}", flush=True)
 
 
@@ -158,7 +161,7 @@ def test_full_size_sampled_parity(name):
                 g_qa, g_k, g_v = oracle.attend_bwd(qa, kk, vv, doa, scale, k_rows=keys)
                 got_qa = to64(res["dq"][a:b, h])
                 _bwd_maxabs(got_qa, g_qa, f"{name} seg {s} head {h} dq, all {b - a} rows")
-                _bwd_fro(got_qa, g_qa, f"{name} seg {s} head {h} dq, all {b - a} rows")
+                _bwd_fro(got_qa, g_qa, f"{name} seg {s} head {h} dq, all {b - a} rows", BWD_REL_FRO_POOLED)
                 print(f"{name} seg {s} head {h}: forward and dQ checked on all {b - a} rows", flush=True)
                 kp = kidx[torch.as_tensor(keys, device="cuda")]
                 for got, ref, nm in ((to64(res["dk"][kp, h]), g_k, "dk"), (to64(res["dv"][kp, h]), g_v, "dv")):
@@ -168,7 +171,7 @@ def test_full_size_sampled_parity(name):
         # whole sample (one head's two dozen rows of a nearly one-hot segment can miss its large entries)
         dq_got, dq_ref = np.concatenate(dq_got), np.concatenate(dq_ref)
         _bwd_maxabs(dq_got, dq_ref, f"{name} seg {s} all heads dq")
-        _bwd_fro(dq_got, dq_ref, f"{name} seg {s} all heads dq")
+        _bwd_fro(dq_got, dq_ref, f"{name} seg {s} all heads dq", BWD_REL_FRO_POOLED)
         # identities that hold at any size, every head: sum_j dK_j = 0, sum_j dV_j = sum_i dO_i
         dk_sum = res["dk"][kidx].double().sum(0)
         dk_abs = res["dk"][kidx].double().abs().sum(0)

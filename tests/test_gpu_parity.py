@@ -3,7 +3,7 @@ small seeded batches that span several tiles and ragged tails, plus the
 invariants exact attention must satisfy on the device itself.
 
 Tolerances: bf16 max|dO| <= 2e-2 and max|dLSE| <= 1e-3 for outputs; backward
-max abs error <= 2e-2 * max(1, max|ref|) and relative Frobenius error <= 2e-2
+max abs error <= 2e-2 * max(1, max|ref|) and relative Frobenius error <= 1e-2
 (see BWD_REL_FRO); fp32 plumbing runs 1e-5 on both.
 """
 import numpy as np
@@ -17,11 +17,12 @@ from tests._gpu import HAVE_GPU, api, to64
 pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not HAVE_GPU, reason="needs a GPU")]
 
 O_TOL, LSE_TOL = 2e-2, 1e-3
-# Backward: the gradients consume the forward output as stored (bf16), and
-# D_i = dO_i . O_i inherits its rounding; for a nearly one-hot softmax
-# (the x4-scaled segments) dS = P (dP - D) is a small difference, and the
-# oracle alone shows a 0.55% relative dQ change from rounding O to bf16.
-BWD_REL_FRO = 2e-2
+# Backward, end to end through the bf16 forward, on whole small batches: the
+# CPU error budget (tests/test_bwd_error_budget.py) puts the chain at 0.24% on
+# unscaled inputs and about 0.6% on x4-scaled ones (a nearly one-hot softmax,
+# where dS = P (dP - D) is a small difference and the bf16-stored O's error
+# through D counts most), so the relative Frobenius bound is 1e-2.
+BWD_REL_FRO = 1e-2
 
 
 def _inputs(d, H, hd, dtype, seed):
@@ -40,6 +41,7 @@ def _check_bwd(got, ref, name):
     if nref > 0:
         rel = np.linalg.norm(got - ref) / nref
         assert rel <= BWD_REL_FRO, f"{name}: relative Frobenius err {rel}"
+        print(f"{name}: rel Frobenius {rel:.3g}", flush=True)
 
 
 def _whole_rows(d):

@@ -159,7 +159,7 @@ def _bwd_tol_check(got, ref, name):
     err = np.abs(got - ref).max()
     assert err <= 2e-2 * max(1.0, np.abs(ref).max()), f"{name}: max abs err {err}"
     nref = np.linalg.norm(ref)
-    assert nref == 0 or np.linalg.norm(got - ref) / nref <= 2e-2, name
+    assert nref == 0 or np.linalg.norm(got - ref) / nref <= 1e-2, name   # the all-blocks path's bound
 
 
 @pytest.mark.parametrize("hd,fill_step", [(128, 0), (64, 2), (128, 1)])
