@@ -39,6 +39,17 @@
  *     tables exist, calls with it only launch kernels (no allocation, copy,
  *     memset or synchronisation), so they may be captured in a HIP graph;
  *     make the first call eagerly, and keep profiling off while capturing.
+ *   - The attention kernels run one workgroup per compute unit and hand out
+ *     a launch's work items at run time through atomic counters in a static
+ *     device array (no allocation): each stream the library is called on
+ *     gets its own counters (up to 64 streams per GPU; calls on further
+ *     streams run one work item per workgroup, with the same results).  So
+ *     calls that overlap on different streams are independent, and calls on
+ *     one stream are ordered.  A captured graph uses the counters of the
+ *     stream it was captured on: do not replay it while calls on that stream
+ *     (or another replay of it) may still run.  Results do not depend on
+ *     which workgroup runs an item.  ZL_STATIC_DISPATCH=1 in the environment
+ *     (read once) selects one work item per workgroup for every call.
  */
 #ifndef ZL_ATTN_H
 #define ZL_ATTN_H

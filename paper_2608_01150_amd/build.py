@@ -14,7 +14,7 @@ OBJ = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(PKG, "libzl_attn.so")
 
 SOURCES = ["zl_host.cpp", "planner.cpp", "fwd_bf16.hip", "fwd_fp32.hip", "merge.hip", "bwd_bf16.hip", "ulysses.hip",
-           "noalloc.hip"]
+           "noalloc.hip", "workq.hip"]
 
 # -packed-fp32-ops keeps hipcc from forming packed fp32 VALU ops.
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=fast",

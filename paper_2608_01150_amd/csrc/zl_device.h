@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "zl_internal.h"
+
 namespace zl {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -237,6 +239,74 @@ __device__ __forceinline__ float xor32_max(float v) {
 __device__ __forceinline__ float xor32_sum(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// ----------------------------------------------------------- work queues
+// Dynamic distribution of a launch's work items over resident workgroups.
+// The work table in dispatch order (dispatch_item) is split into 8 queues:
+// queue y holds the dispatch positions y, y+8, y+16, ..., which the hardware's
+// round-robin placement of workgroups would send to XCD y.  Workgroup b
+// (grid G <= n) first runs position b, i.e. the first round of a
+// one-item-per-workgroup launch; afterwards it claims further positions of
+// its own XCD's queue with a device-scope atomic counter, and once that queue
+// is empty those of the other XCDs' queues in turn.  The XCDs of one GPU run
+// at different speeds (several percent apart under load), and a fixed share
+// of the items per XCD leaves the fast ones idle while the slowest finishes;
+// here an XCD that runs ahead takes over the tail of the others' queues.
+// ctr[y] counts the claims on queue y beyond its first round and ctr[8] the
+// workgroups that have finished; the last one to finish resets all nine, so
+// the next launch that uses the same counters finds them at zero.
+
+__device__ __forceinline__ int xcd_id() {
+  uint32_t r;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(r));
+  return (int)(r & 7u);
+}
+
+// Claim of the next position of the queue this workgroup is working on
+// (queue (xcd + tries) % 8), issued ahead of need so that its latency
+// overlaps work; its result goes to wq_next as `pending`.
+__device__ __forceinline__ int wq_claim(int* ctr, int tries) { return atomicAdd(&ctr[(xcd_id() + tries) & 7], 1); }
+
+// Work-table index of this workgroup's next item, or -1 when every queue is
+// empty.  *tries (workgroup state, in LDS) counts the queues found empty;
+// pending is a claim from wq_claim on the current queue, or -1.
+__device__ __forceinline__ int wq_next(int* ctr, int n, int chunk, int* tries, int pending) {
+  int t = *tries;
+  const int grid = (int)gridDim.x;
+  while (t < 8) {
+    const int y = (xcd_id() + t) & 7;
+    const int len = (n - y + 7) >> 3;      // positions y + 8k below n
+    const int first = (grid - y + 7) >> 3;  // of those, taken by the first round
+    const int k = first + (pending >= 0 ? pending : atomicAdd(&ctr[y], 1));
+    pending = -1;
+    if (k < len) {
+      *tries = t;
+      return dispatch_item(8 * k + y, n, chunk);
+    }
+    ++t;
+  }
+  *tries = t;
+  return -1;
+}
+
+// Called once per workgroup after its last item.
+__device__ __forceinline__ void wq_finish(int* ctr) {
+  if ((unsigned)atomicAdd(&ctr[8], 1) == gridDim.x - 1u) {
+#pragma unroll
+    for (int y = 0; y < 9; ++y) atomicExch(&ctr[y], 0);
+  }
+}
+
+// The launch's parameters read afresh from the kernel-argument segment, by
+// scalar loads at the point of use.  A persistent kernel would otherwise hold
+// arguments that only an item's epilogue needs in registers across its whole
+// item loop.
+template <class P>
+__device__ __forceinline__ const __attribute__((address_space(4))) P* kernargs() {
+  auto* k = (const __attribute__((address_space(4))) P*)__builtin_amdgcn_kernarg_segment_ptr();
+  asm volatile("" : "+s"(k));
+  return k;
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }

@@ -610,6 +610,7 @@ zl_status zl_attn_fwd_ex(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dtyp
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
   p.xcd_chunk = xcd_chunk(sh);
+  if ((st = zl::stream_counters(s, &p.wq)) != ZL_OK) return st;
   hipError_t e = timed(ZL_K_FWD, s, [&] {
     return dt == ZL_BF16 ? zl::launch_fwd_bf16(p, hd, s) : zl::launch_fwd_fp32(p, hd, s);
   });
@@ -658,6 +659,7 @@ zl_status zl_attn_fwd_step(const zl_seg_desc* desc, int32_t H, int32_t hd, zl_dt
   p.step_last = last;
   p.o_acc = o_acc;
   p.lse_acc = lse_acc;
+  if ((st = zl::stream_counters(s, &p.wq)) != ZL_OK) return st;
   hipError_t e = timed(ZL_K_FWD, s, [&] {
     return dt == ZL_BF16 ? zl::launch_fwd_bf16(p, hd, s) : zl::launch_fwd_fp32(p, hd, s);
   });
@@ -876,6 +878,11 @@ zl_status launch_bwd(const BwdCall& c, const Shape& sh, const void* tables, size
   p.step_first = first ? 1 : 0;
   p.step_last = last ? 1 : 0;
   p.dq_acc = c.dq_acc;
+  int* wq = nullptr;
+  const zl_status wst = zl::stream_counters(s, &wq);
+  if (wst != ZL_OK) return wst;
+  p.wq_kv = wq ? wq + zl::kWqPerLaunch : nullptr;
+  p.wq_q = wq ? wq + 2 * zl::kWqPerLaunch : nullptr;
   const int hd = c.hd;
   hipError_t e = timed(ZL_K_BWD_PRE, s, [&] { return zl::launch_bwd_bf16(p, hd, 0, s); });
   if (e == hipSuccess) e = timed(ZL_K_BWD_DKDV, s, [&] { return zl::launch_bwd_bf16(p, hd, 1, s); });

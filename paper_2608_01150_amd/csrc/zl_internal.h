@@ -73,6 +73,9 @@ struct FwdParams {
   float* o_acc;          // [Tq, H, d] fp32
   float* lse_acc;        // [Tq, H] fp32
   int32_t part_bf16;     // SHARD partials stored as bf16 (rounded once) instead of fp32
+  // Work-queue counters of this launch (the stream's, see stream_counters),
+  // or NULL for one item per workgroup in dispatch order (grid = n_items).
+  int* wq;
 };
 
 struct MergeSeg {
@@ -122,7 +125,24 @@ struct BwdParams {
   int32_t step_first;    // the accumulator starts from this block
   int32_t step_last;     // the accumulated dQ (scaled, bf16) goes to dq
   float* dq_acc;         // [Tq, H, d] fp32
+  int* wq_kv;            // work-queue counters of the dK/dV and dQ launches, or NULL (see FwdParams::wq)
+  int* wq_q;
 };
+
+// Work-queue counters: each stream the library launches on gets one block of
+// kWqInts ints in a static device array (zero at load; every launch leaves
+// its counters at zero), kWqPerLaunch per kernel.  *out is NULL when the
+// device's kWqSlots blocks are all taken by other streams: the kernels then
+// run one item per workgroup.  Caller holds the library lock.
+constexpr int kWqPerLaunch = 16;
+constexpr int kWqInts = 4 * kWqPerLaunch;  // forward, dK/dV, dQ, spare
+constexpr int kWqSlots = 64;
+zl_status stream_counters(hipStream_t s, int** out);
+
+// Grid of a launch of `kernel` (block threads, static LDS) over n_items with
+// work queues: n_items when ctr is NULL, else min(n_items, resident
+// workgroups of the device).
+int launch_grid(const void* kernel, int block, int n_items, const int* ctr);
 
 hipError_t launch_fwd_bf16(const FwdParams& p, int head_dim, hipStream_t s);
 hipError_t launch_fwd_fp32(const FwdParams& p, int head_dim, hipStream_t s);
