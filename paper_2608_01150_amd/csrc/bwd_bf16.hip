@@ -425,8 +425,8 @@ __device__ __forceinline__ void dq_store(const __attribute__((address_space(4)))
 }
 
 // ------------------------------------------------------------------ dQ
-// One workgroup of 8 waves (two per SIMD, 32 query rows each) per item of up
-// to 256 query rows of one head.  A segment's K/V ranges are consecutive rows
+// An item is up to 256 query rows of one head (8 waves, two per SIMD, 32 query
+// rows each).  A segment's K/V ranges are consecutive rows
 // of K and V, and dQ sums over all of them against the final LSE, so the item
 // streams the segment's keys [k_start, k_start + k_len) as one range: block
 // boundaries play no part in the backward.  128-key K/V tiles rotate through
@@ -619,26 +619,24 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(BwdParams p) {
     // item without keys (a shard whose blocks are all empty) runs one step on
     // an all-zero tile, which adds exactly zero (K = 0), rather than branching
     // around the loop.
-    {
-      fetch(0, ks0, vs0);
-      for (int kt = 0;;) {
-        wait_vmem();
-        __syncthreads();  // tile in buffers 0 complete; buffers 1 no longer read
-        fetch_spread(kt + TN, ks1, vs1);
-        if (kt + TN >= it.k_len) claim_ahead();
-        tile(ks0, vs0, kt);
-        kt += TN;
-        if (kt >= it.k_len) break;
-        wait_vmem();
-        __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
-        fetch_spread(kt + TN, ks0, vs0);
-        if (kt + TN >= it.k_len) claim_ahead();
-        tile(ks1, vs1, kt);
-        kt += TN;
-        if (kt >= it.k_len) break;
-      }
-      wait_vmem();  // the lookahead loads must land before the LDS is reused
+    fetch(0, ks0, vs0);
+    for (int kt = 0;;) {
+      wait_vmem();
+      __syncthreads();  // tile in buffers 0 complete; buffers 1 no longer read
+      fetch_spread(kt + TN, ks1, vs1);
+      if (kt + TN >= it.k_len) claim_ahead();
+      tile(ks0, vs0, kt);
+      kt += TN;
+      if (kt >= it.k_len) break;
+      wait_vmem();
+      __syncthreads();  // tile in buffers 1 complete; buffers 0 no longer read
+      fetch_spread(kt + TN, ks0, vs0);
+      if (kt + TN >= it.k_len) claim_ahead();
+      tile(ks1, vs1, kt);
+      kt += TN;
+      if (kt >= it.k_len) break;
     }
+    wait_vmem();  // the lookahead loads must land before the LDS is reused
 
     // dq[db][i] is (d = db*32 + 16*(i/8) + 8g + i%8, query qr).
     if (q_ok) dq_store<D>(kernargs<BwdParams>(), it, qrow, g, dq);
