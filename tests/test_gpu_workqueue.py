@@ -33,12 +33,12 @@ pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not HAVE_GPU, reason="needs a 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def batch():
+def batch(head_dim=128):
     """WHOLE segments of ragged lengths plus a three-block SHARD, 48 heads:
     768 forward, 1104 dK/dV and 576 dQ items, all above the 256 CUs."""
     segs = [("whole", 600, 0), ("whole", 1000, 10_000), ("whole", 333, 20_000), ("whole", 64, 30_000),
             ("shard", 300, 40_000, [(200, 40_000, 0), (250, 50_000, 1), (130, 60_000, 2)])]
-    return W.build_segments("workqueue-test", 48, 128, segs, 20261202)
+    return W.build_segments("workqueue-test", 48, head_dim, segs, 20261202)
 
 
 def inputs(w, dev):
@@ -84,9 +84,10 @@ def check_equal(ref, got, what):
         assert np.array_equal(a, b), f"{what}: {n} differs in {(a != b).sum()} of {a.size} elements"
 
 
-def test_dynamic_dispatch_equals_static_dispatch():
+@pytest.mark.parametrize("head_dim", [128, 64])
+def test_dynamic_dispatch_equals_static_dispatch(head_dim):
     dev = torch.device("cuda:0")
-    w = batch()
+    w = batch(head_dim)
     desc = api.SegDesc.of(w)
     items, _ = api.plan_dump(desc, w.num_heads, w.head_dim, torch.bfloat16, api.ZL_OP_FWD)
     assert len(items) > torch.cuda.get_device_properties(0).multi_processor_count, "batch must exceed one round"
@@ -95,7 +96,7 @@ def test_dynamic_dispatch_equals_static_dispatch():
     with tempfile.TemporaryDirectory() as tmp:
         path = os.path.join(tmp, "static.npz")
         env = dict(os.environ, ZL_STATIC_DISPATCH="1")
-        r = subprocess.run([sys.executable, "-m", "tests.test_gpu_workqueue", path], cwd=ROOT, env=env,
+        r = subprocess.run([sys.executable, "-m", "tests.test_gpu_workqueue", path, str(head_dim)], cwd=ROOT, env=env,
                            capture_output=True, text=True, timeout=600)
         assert r.returncode == 0, r.stdout[-2000:] + r.stderr[-2000:]
         st = np.load(path)
@@ -142,7 +143,7 @@ def test_concurrent_streams_have_their_own_counters():
 if __name__ == "__main__":
     # Child process of test_dynamic_dispatch_equals_static_dispatch (run with ZL_STATIC_DISPATCH=1).
     dev = torch.device("cuda:0")
-    w = batch()
+    w = batch(int(sys.argv[2]))
     desc = api.SegDesc.of(w)
     res = run(w, desc, *inputs(w, dev), *alloc(w, desc, dev))
     torch.cuda.synchronize()

@@ -1,7 +1,8 @@
 """zl_attn_bwd_noalloc, the backward for callers that cannot allocate: its work tables and workspace
 sit in the library's static device scratch.  It must give zl_attn_bwd's results bit for bit (the same
-work items on the same kernels) on consecutive calls that reuse the scratch, the second one smaller,
-and reject a batch that does not fit the scratch before enqueueing anything."""
+work items on the same kernels) on consecutive calls that reuse the scratch, the second one smaller
+and the third with more work items than resident workgroups, and reject a batch that does not fit the
+scratch before enqueueing anything."""
 import numpy as np
 import pytest
 import torch
@@ -43,6 +44,9 @@ def test_noalloc_backward_matches_backward_on_consecutive_calls():
     small = _descs.desc(cu_q=(0, 90, 130), kind=(0, 1), kv_first=(0, 1), kv_count=(1, 2),
                         cu_k=(0, 90, 140, 170), block_index=(0, 1, 0), num_slots=2)
     _compare(small, 2, 64, 72)
+    # third call, 96 heads: 864 dK/dV and 384 dQ items, more than the GPU's resident workgroups, so most
+    # items are handed out at run time through the kernels' work queues
+    _compare(_descs.mixed_small(), 96, 128, 73)
 
 
 def test_noalloc_rejects_a_batch_beyond_the_scratch():
