@@ -47,7 +47,7 @@ constexpr float kSumBound = 0x1p64f;
 // query and stores it by the item's kind.  o[db][i] is (d = db*32 +
 // 16*(i/8) + 8*g + i%8, query qr); m_run is the running maximum (log2
 // units), l_part this lane's half of the row sum of the exponentials and
-// l_rnd its half of the sum of the same values rounded to bf16, as they
+// l_rnd the whole row's sum of the same values rounded to bf16, as they
 // entered O += P V.  The output is normalised by the rounded sum, so its
 // weights sum to one exactly: the rounding of a dominant P (any value in
 // [1, 2^64) against a running maximum that a later key exceeds) cancels
@@ -57,7 +57,7 @@ __device__ __forceinline__ void fwd_store(const __attribute__((address_space(4))
                                           bool q_ok, int g, const f32x16 (&o)[D / 32], float m_run, float l_part,
                                           float l_rnd) {
   const auto& p = *pp;
-  const float l = xor32_sum(l_part), lr = xor32_sum(l_rnd);
+  const float l = xor32_sum(l_part), lr = l_rnd;
   const float inv = lr > 0.f ? 1.f / lr : 0.f;
   const float lse = l > 0.f ? (m_run + __log2f(l)) * kLn2 : -INFINITY;
   if (!q_ok) return;
@@ -187,7 +187,16 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
     // vmcnt wait there (which would also drain the in-flight tile DMAs).
     __builtin_amdgcn_s_waitcnt(0);
 
-    float m_run = kNegBig, l_part = 0.f, l_rnd = 0.f;
+    float m_run = kNegBig, l_part = 0.f;
+    // The rounded sum comes from the matrix core: one mfma16 per 16-key P word
+    // (the PV B operand, lane l holding 8 keys of query l%32) against a 0/1
+    // selector A.  Lane l of A is all ones where bit 4 of l equals bit 2, so
+    // output row m sums the lanes of query (column + 16 * ((m/4) % 2)) over
+    // both key halves, and every register of lane l ends up holding the full
+    // rounded sum of query l%32.
+    f32x4 racc = f32x4{0.f, 0.f, 0.f, 0.f};
+    const uint32_t selw = ((lane >> 4) & 1) == ((lane >> 2) & 1) ? 0x3F803F80u : 0u;
+    const u32x4 rsel = {selw, selw, selw, selw};
     f32x16 o[D / 32];
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) o[db] = f32x16{};
@@ -250,9 +259,9 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       // s[kb][i] is the raw score of (key kb*32 + 16*(i/8) + 8*g + i%8, query qr).
       f32x16 s[2];
       u32x4 pb[2][2];
-      // Each block's two sums in two partial accumulators (words of even and
+      // Each block's sum in two partial accumulators (words of even and
       // odd c), which halves their dependency chains.
-      float lsum[2][2] = {}, lrnd[2][2] = {};
+      float lsum[2][2] = {};
       // Keys past the range on a partial tile: score -inf, exact at any positive scale.
       auto mask = [&](int kb) {
         if (nvalid < BN) {
@@ -269,7 +278,6 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
         const float e1 = fast_exp2(fmaf(s[kb][2 * c + 1], p.scale_log2, -m_run));
         lsum[kb][c & 1] += e0 + e1;
         pb[kb][c >> 2][c & 3] = pack_bf16(e0, e1);
-        lrnd[kb][c & 1] = sum_bf16x2(pb[kb][c >> 2][c & 3], lrnd[kb][c & 1]);
       };
       // The slow path of block kb (see kSumBound): when it is taken for block 1,
       // block 0 has entered O already, and the rescale covers it there.
@@ -282,20 +290,19 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
         const float alpha = fast_exp2(m_run - m_new);
         m_run = m_new;
         l_part *= alpha;
-        l_rnd *= alpha;
+        racc *= alpha;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
           for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
         }
-        lsum[kb][0] = lsum[kb][1] = lrnd[kb][0] = lrnd[kb][1] = 0.f;
+        lsum[kb][0] = lsum[kb][1] = 0.f;
 #pragma unroll
         for (int c = 0; c < 8; ++c) expo(kb, c);
       };
       auto block_done = [&](int kb) {
         if (__any(lsum[kb][0] + lsum[kb][1] > kSumBound)) block_fix(kb);
         l_part += lsum[kb][0] + lsum[kb][1];
-        l_rnd += lrnd[kb][0] + lrnd[kb][1];
       };
 
       u32x4 ring[PF];
@@ -326,7 +333,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
           for (int c = c0; c < c1; ++c) {
             expo(0, c);
-            asm volatile("" : "+v"(pb[0][c >> 2][c & 3]), "+v"(lsum[0][c & 1]), "+v"(lrnd[0][c & 1]));
+            asm volatile("" : "+v"(pb[0][c >> 2][c & 3]), "+v"(lsum[0][c & 1]));
           }
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -349,12 +356,14 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
           for (int c = m * 8 / (NP / 2); c < (m + 1) * 8 / (NP / 2); ++c) {
             expo(1, c);
-            asm volatile("" : "+v"(pb[1][c >> 2][c & 3]), "+v"(lsum[1][c & 1]), "+v"(lrnd[1][c & 1]));
+            asm volatile("" : "+v"(pb[1][c >> 2][c & 3]), "+v"(lsum[1][c & 1]));
           }
         }
         if (m == NP / 2) block_done(1);
         const int kb = m / (NP / 2), db = (m % (NP / 2)) >> 1, s2 = m & 1;
         o[db] = mfma32(a, pb[kb][s2], o[db]);
+        // The rounded sum of each P word, after its block's sum check.
+        if ((m % (NP / 2)) % (NP / 4) == 1) racc = mfma16(rsel, pb[kb][(m % (NP / 2)) / (NP / 4)], racc);
         __builtin_amdgcn_sched_barrier(0);
       }
       __builtin_amdgcn_s_setprio(0);
@@ -412,7 +421,7 @@ __global__ __launch_bounds__(NT, 1) void fwd_bf16_kernel(FwdParams p) {
       wait_vmem();  // the lookahead loads must land before the workgroup's LDS is released
     }
 
-    fwd_store<D>(kernargs<FwdParams>(), it, qr, q_ok, g, o, m_run, l_part, l_rnd);
+    fwd_store<D>(kernargs<FwdParams>(), it, qr, q_ok, g, o, m_run, l_part, racc[0]);
     const auto* pk = kernargs<FwdParams>();
     if (tid == 0) s_item[parity] = pk->wq ? wq_next(pk->wq, pk->n_items, pk->xcd_chunk, &s_tries, pending) : -1;
     pending = -1;

@@ -24,6 +24,15 @@ __device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f
                                                  0, 0, 0);
 }
 
+// D(16x16 fp32) += A(16x32 bf16) * B(32x16 bf16), half the cycles of mfma32.
+// Lane l supplies row l%16 of A and column l%16 of B, each as the 8 values of
+// k-group l/16; D register i of lane l is element (row 4*(l/16) + i, column
+// l%16).
+__device__ __forceinline__ f32x4 mfma16(const u32x4& a, const u32x4& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                 0, 0, 0);
+}
+
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -31,12 +40,6 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 // (one v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
-}
-
-// acc + lo + hi of a packed bf16 pair (one v_dot2c_f32_bf16 against 1.0).
-__device__ __forceinline__ float sum_bf16x2(uint32_t w, float acc) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), __builtin_bit_cast(bf16x2, 0x3F803F80u), acc,
-                                         false);
 }
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
