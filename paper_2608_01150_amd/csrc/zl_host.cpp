@@ -6,8 +6,8 @@
 // work items and orders them longest-processing-time first: cost = rows x keys,
 // the quadratic attention work of Sec. II-A.  Ties follow segment order, as
 // Sec. IV-D sorts a rank's segments by split degree with a fixed placement
-// order settling ties.  With the hardware dispatcher handing each free compute
-// unit the next workgroup in this order, the launch runs as greedy list
+// order settling ties.  With each free compute unit taking the next item in
+// this order (from the kernels' work queues), the launch runs as greedy list
 // scheduling of the items in LPT order: each item goes, largest first, to the
 // least-loaded place, as the paper's Filler Packing (Eq. 8) places fillers
 // across ranks.
