@@ -369,6 +369,10 @@ def main():
     from paper_2608_01150_amd import workloads as W
 
     w = W.get(args.workload)
+    if args.mode in ("ring", "gather") and not any(w.kind[s] == W.SHARD for s in range(w.num_segments)):
+        print(f"--mode {args.mode} delivers a shard's K/V blocks step by step or concatenated; the workload "
+              f"{w.name} has no shard segments (use --workload c4 or c5).", file=sys.stderr)
+        sys.exit(2)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     desc = api.SegDesc.of(w)

@@ -22,3 +22,10 @@ def test_help_lists_the_contract_flags():
     assert r.returncode == 0
     for flag in ("--gpus", "--steps", "--warmup", "--workload", "--mode"):
         assert flag in r.stdout
+
+
+def test_block_delivery_modes_need_a_shard():
+    for mode in ("ring", "gather"):
+        r = _run("--workload", "c3", "--mode", mode, "--steps", "1", "--warmup", "0", "--no-cpu-baseline")
+        assert r.returncode == 2
+        assert "no shard segments" in r.stderr and r.stdout.strip() == ""
